@@ -1,0 +1,50 @@
+/*
+ * hs_kernel.h - single-kernel entry points of the stage engine.
+ *
+ * These run one of the engine's HIP kernels on caller-owned device buffers,
+ * exactly as the stage forward pass launches it. They exist so that each
+ * kernel can be checked against a reference and timed on its own; serving
+ * goes through hs.h. All pointers are device pointers owned by the caller;
+ * `stream` is a hipStream_t (NULL = the null stream). Work is asynchronous.
+ * Shapes the kernel does not support return HS_EINVAL before any launch.
+ */
+#ifndef HS_KERNEL_H
+#define HS_KERNEL_H
+
+#include <stdint.h>
+
+#include "hs.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Y[m][n] = epilogue(sum_k X[m][k] W[n][k]) with fp32 accumulation; X, W bf16,
+ * row-major with row strides ldx / ldw (elements). epi: 0 store bf16; 1 add
+ * the bf16 residual R (row stride ldr; may alias Y); 2 SwiGLU on gate/up rows
+ * interleaved in groups of 16, Y has N/2 columns; 3 store float32. Requires
+ * K % 8 == 0, N % 16 == 0 (N % 32 for SwiGLU), 16-byte aligned X, W, Y. This
+ * is the projection arithmetic of every decoder layer (QKV, O, gate/up,
+ * down) and of the LM head. */
+hs_status hs_k_gemm(const void* X, int64_t ldx, const void* W, int64_t ldw, void* Y,
+                    int64_t ldy, const void* R, int64_t ldr, int32_t M, int32_t N, int32_t K,
+                    int32_t epi, void* stream);
+
+/* Causal grouped-query attention over packed sequences (the attention of the
+ * prefill pass). qkv: bf16 [T][(n_heads + 2 n_kv_heads) head_dim] holding
+ * post-RoPE q, k, v per token; out: bf16 [T][n_heads head_dim]; cu_seqlens:
+ * HOST int32 [n_seqs + 1] token offsets (cu[0] = 0, cu[n] = T). */
+hs_status hs_k_attn_prefill(const void* qkv, void* out, const int32_t* cu_seqlens,
+                            int32_t n_seqs, int32_t n_heads, int32_t n_kv_heads,
+                            int32_t head_dim, void* stream);
+
+/* RMSNorm of `rows` rows of width `hidden`: out = x / sqrt(mean(x^2) + eps) * g,
+ * bf16 in and out, float32 arithmetic. */
+hs_status hs_k_rmsnorm(const void* x, const void* g, void* out, int32_t rows, int32_t hidden,
+                       float eps, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HS_KERNEL_H */

@@ -1,0 +1,90 @@
+// Host-side launchers of the engine's HIP kernels. Every launcher checks the
+// shapes its kernel assumes and returns hipErrorInvalidValue instead of
+// launching when they do not hold.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hs {
+
+typedef uint16_t bf16_t;
+
+// Epilogues of Y[m][n] = sum_k X[m][k] * W[n][k] (fp32 accumulation).
+enum Epi : int {
+  EPI_STORE = 0,   // Y = bf16(acc)
+  EPI_RESID = 1,   // Y = bf16(R + acc); R may alias Y
+  EPI_SWIGLU = 2,  // W rows interleave 16 gate / 16 up rows; Y[m][f] = bf16(silu(g) * u), width N/2
+  EPI_F32 = 3      // Y = acc as float32
+};
+
+struct GemmArgs {
+  const bf16_t* X; int64_t ldx;  // [M][K] activations, row stride ldx elements
+  const bf16_t* W; int64_t ldw;  // [N][K] weights
+  void* Y; int64_t ldy;          // output, row stride ldy elements (of its type)
+  const bf16_t* R; int64_t ldr;  // residual input for EPI_RESID
+  int M, N, K;
+};
+
+// Describes what was launched (for timing).
+struct LaunchInfo {
+  const char* name;
+  double flops;
+  double bytes;
+};
+
+hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info);
+
+hipError_t embed(const int32_t* tok, const bf16_t* E, int vocab, int hidden, int n_tok,
+                 bf16_t* out, hipStream_t s, LaunchInfo* info);
+
+// out[r] = rmsnorm(x[rows ? rows[r] : r]) * g
+hipError_t rmsnorm(const bf16_t* x, int64_t ldx, const int32_t* rows, int n_rows, int hidden,
+                   const bf16_t* g, float eps, bf16_t* out, int64_t ldo, hipStream_t s,
+                   LaunchInfo* info);
+
+struct RopeKvArgs {
+  bf16_t* qkv; int64_t ld;       // [T][ld]: q heads, k heads, v heads
+  const int32_t* pos;            // [T] position of each token
+  const int32_t* slot;           // [T] physical KV slot (block * 16 + offset)
+  const float* cos_t; const float* sin_t;  // [max_pos][D/2]
+  bf16_t* pool;                  // this layer's pool [blocks][2][n_kv][16][D]
+  int T, n_heads, n_kv_heads, D, max_pos;
+};
+hipError_t rope_kv(const RopeKvArgs& a, hipStream_t s, LaunchInfo* info);
+
+struct AttnPrefillArgs {
+  const bf16_t* qkv; int64_t ld;  // post-RoPE q, k and v
+  bf16_t* out; int64_t ldo;       // [T][n_heads * D]
+  const int32_t* cu;              // [n_seqs + 1] token offsets
+  const int32_t* tiles;           // [n_tiles][2] (sequence, first query row)
+  int n_tiles, n_heads, n_kv_heads, D;
+  double flops;                   // unmasked-pair flops, for reporting
+};
+hipError_t attn_prefill(const AttnPrefillArgs& a, hipStream_t s, LaunchInfo* info);
+
+constexpr int kDecodeSplit = 256;  // tokens per split of the decode attention
+
+struct AttnDecodeArgs {
+  const bf16_t* q; int64_t ldq;   // [B][ldq], query heads at column h * D
+  const bf16_t* pool;             // layer pool [blocks][2][n_kv][16][D]
+  const int32_t* block_table;     // [B][max_blocks]
+  const int32_t* ctx;             // [B] cached positions including the new one
+  float* part_o;                  // [B][n_heads][max_splits][D]
+  float* part_ml;                 // [B][n_heads][max_splits][2]
+  bf16_t* out; int64_t ldo;       // [B][n_heads * D]
+  int B, n_heads, n_kv_heads, D, max_blocks, max_splits, call_splits;
+  double kv_bytes;                // bytes of K/V read, for reporting
+};
+hipError_t attn_decode(const AttnDecodeArgs& a, hipStream_t s, LaunchInfo* info_split,
+                       LaunchInfo* info_combine);
+
+hipError_t argmax_rows(const float* logits, int n_rows, int n_cols, int32_t* out, hipStream_t s,
+                       LaunchInfo* info);
+
+// Copy `n_units` KV units (a K block followed by its V block, unit_bytes each);
+// slots at or past valid[u] are written as zero when zero_tail is set.
+hipError_t kv_copy(const uint64_t* src, const uint64_t* dst, const int32_t* valid, int n_units,
+                   int64_t unit_bytes, int D, int zero_tail, hipStream_t s, LaunchInfo* info);
+
+}  // namespace hs

@@ -1,0 +1,365 @@
+// Causal attention for prefill (flash-style, MFMA) and split-K paged decode.
+//
+// Prefill reads post-RoPE q, k and v straight from the QKV GEMM output (the
+// whole prompt is in the call), one workgroup per (64-query tile, head).
+// Decode reads the paged KV pools through each sequence's block table; the
+// context is cut into fixed 256-token splits, so the split count depends on
+// the context length only and the result is deterministic.
+#include "hs_device.h"
+#include "hs_kernels.h"
+
+namespace hs {
+
+// ------------------------------------------------------------------ prefill
+//
+// Wave w of the workgroup owns queries q0 + 16w .. q0 + 16w + 15. Scores are
+// computed transposed, S^T[key][query] = K Q^T, so that each lane holds 16
+// scores of ONE query (4 per 16-key subtile); the softmax statistics of a
+// query then live in the 4 lanes l, l+16, l+32, l+48. P^T feeds the second
+// MFMA as its B operand with the key order of each 32-key step permuted
+// (lane group g, element e -> key 4g+e for e<4, 16+4g+e-4 otherwise); V^T is
+// read from LDS with the same permutation, so the product is unchanged.
+
+template <int D>
+__global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefillArgs a, float scale_log2) {
+  constexpr int KB = 64;        // keys per block
+  constexpr int LK = D + 8;     // padded K row in LDS
+  constexpr int LV = KB + 2;    // padded V^T row in LDS (33 dwords: conflict-free writes)
+  constexpr int CPK = D / 8;    // 16-byte chunks per key row
+  __shared__ __attribute__((aligned(16))) bf16_t sK[KB * LK];
+  __shared__ __attribute__((aligned(16))) bf16_t sVt[D * LV];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int seq = a.tiles[2 * blockIdx.x], q0 = a.tiles[2 * blockIdx.x + 1];
+  const int h = blockIdx.y;
+  const int kh = h / (a.n_heads / a.n_kv_heads);
+  const int base = a.cu[seq], len = a.cu[seq + 1] - base;
+  const int fr = lane & 15, g = lane >> 4;
+
+  const int qrow = q0 + wave * 16 + fr;  // this lane's query (position in sequence)
+  bf16x8_v qf[D / 32];
+#pragma unroll
+  for (int ks = 0; ks < D / 32; ++ks) {
+    pack8 v = zero8();
+    if (qrow < len) v = ld16(a.qkv + (int64_t)(base + qrow) * a.ld + h * D + ks * 32 + g * 8);
+    qf[ks] = as_bf16x8(v);
+  }
+
+  f32x4_v o[D / 16];
+#pragma unroll
+  for (int i = 0; i < D / 16; ++i) o[i] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;
+
+  const int kend = min(len, q0 + 64);
+  const int n_kb = (kend + KB - 1) / KB;
+  const bf16_t* kbase = a.qkv + (int64_t)base * a.ld + (a.n_heads + kh) * D;
+  const bf16_t* vbase = a.qkv + (int64_t)base * a.ld + (a.n_heads + a.n_kv_heads + kh) * D;
+
+  for (int kb = 0; kb < n_kb; ++kb) {
+    const int k0 = kb * KB;
+    __syncthreads();
+    // K block, row-major [key][d]
+#pragma unroll
+    for (int i = 0; i < KB * CPK / 256; ++i) {
+      const int c = tid + i * 256, key = c / CPK, col = (c % CPK) * 8;
+      pack8 v = zero8();
+      if (k0 + key < len) v = ld16(kbase + (int64_t)(k0 + key) * a.ld + col);
+      st16(&sK[key * LK + col], v);
+    }
+    // V block, transposed [d][key]; a wave covers 16 keys x 4 chunks
+#pragma unroll
+    for (int i = 0; i < KB * CPK / 256; ++i) {
+      const int c = tid + i * 256;
+      const int key = (c & 15) + 16 * (c / (16 * CPK)), col = ((c >> 4) % CPK) * 8;
+      pack8 v = zero8();
+      if (k0 + key < len) v = ld16(vbase + (int64_t)(k0 + key) * a.ld + col);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        sVt[(col + 2 * e) * LV + key] = (bf16_t)(v.w[e] & 0xFFFFu);
+        sVt[(col + 2 * e + 1) * LV + key] = (bf16_t)(v.w[e] >> 16);
+      }
+    }
+    __syncthreads();
+
+    // S^T for 4 subtiles of 16 keys
+    f32x4_v s[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      s[t] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < D / 32; ++ks) {
+        const bf16x8_v kf = as_bf16x8(ld16(&sK[(t * 16 + fr) * LK + ks * 32 + g * 8]));
+        s[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ks], s[t], 0, 0, 0);
+      }
+    }
+    // mask, scale, block max
+    float bmax = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int key = k0 + t * 16 + g * 4 + e;
+        float v = s[t][e] * scale_log2;
+        if (key > qrow || key >= len) v = -INFINITY;
+        s[t][e] = v;
+        bmax = fmaxf(bmax, v);
+      }
+    bmax = fmaxf(bmax, __shfl_xor(bmax, 16, 64));
+    bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
+    const float m_new = fmaxf(m_run, bmax);  // finite: key k0 <= every query of the tile
+    const float corr = fast_exp2(m_run - m_new);
+    m_run = m_new;
+    float psum = 0.f;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float p = fast_exp2(s[t][e] - m_new);
+        s[t][e] = p;
+        psum += p;
+      }
+    l_run = l_run * corr + psum;
+#pragma unroll
+    for (int i = 0; i < D / 16; ++i) o[i] *= corr;
+
+    // O^T += V^T P^T over two 32-key steps
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      pack8 pb;
+      pb.w[0] = pack2bf(s[2 * st][0], s[2 * st][1]);
+      pb.w[1] = pack2bf(s[2 * st][2], s[2 * st][3]);
+      pb.w[2] = pack2bf(s[2 * st + 1][0], s[2 * st + 1][1]);
+      pb.w[3] = pack2bf(s[2 * st + 1][2], s[2 * st + 1][3]);
+      const bf16x8_v pf = as_bf16x8(pb);
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) {
+        const uint32_t* row = reinterpret_cast<const uint32_t*>(&sVt[(dt * 16 + fr) * LV]);
+        const int k1 = (st * 32 + g * 4) >> 1, k2 = (st * 32 + 16 + g * 4) >> 1;
+        pack8 vb;
+        vb.w[0] = row[k1];
+        vb.w[1] = row[k1 + 1];
+        vb.w[2] = row[k2];
+        vb.w[3] = row[k2 + 1];
+        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vb), pf, o[dt], 0, 0, 0);
+      }
+    }
+  }
+
+  float l_tot = l_run + __shfl_xor(l_run, 16, 64);
+  l_tot += __shfl_xor(l_tot, 32, 64);
+  if (qrow >= len) return;
+  const float inv = 1.0f / l_tot;
+  bf16_t* orow = a.out + (int64_t)(base + qrow) * a.ldo + h * D;
+#pragma unroll
+  for (int dt = 0; dt < D / 16; ++dt) {
+    uint2 w;
+    w.x = pack2bf(o[dt][0] * inv, o[dt][1] * inv);
+    w.y = pack2bf(o[dt][2] * inv, o[dt][3] * inv);
+    *reinterpret_cast<uint2*>(orow + dt * 16 + g * 4) = w;
+  }
+}
+
+hipError_t attn_prefill(const AttnPrefillArgs& a, hipStream_t s, LaunchInfo* info) {
+  if (a.n_tiles <= 0) return hipSuccess;
+  if ((a.D != 64 && a.D != 128) || a.n_kv_heads <= 0 || a.n_heads % a.n_kv_heads) return hipErrorInvalidValue;
+  if ((a.ld % 8) || (a.ldo % 4)) return hipErrorInvalidValue;
+  const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)a.D));
+  dim3 grid(a.n_tiles, a.n_heads);
+  if (a.D == 128)
+    hipLaunchKernelGGL(attn_prefill_kernel<128>, grid, dim3(256), 0, s, a, scale_log2);
+  else
+    hipLaunchKernelGGL(attn_prefill_kernel<64>, grid, dim3(256), 0, s, a, scale_log2);
+  if (info) {
+    info->name = a.D == 128 ? "attn_prefill_d128" : "attn_prefill_d64";
+    info->flops = a.flops;
+    info->bytes = 0;
+  }
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------- decode
+//
+// One workgroup per (split, kv head, sequence). D/8 lanes share a token (one
+// 16-byte chunk each), so 256 threads cover 2048/D tokens per pass; every
+// thread keeps an online softmax over its tokens for the G query heads of
+// the KV head, and the token groups are merged through LDS at the end.
+
+template <int D, int G>
+__global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a, float scale_log2) {
+  constexpr int LPT = D / 8;        // lanes per token
+  constexpr int TPP = 256 / LPT;    // tokens per pass
+  constexpr int PASSES = kDecodeSplit / TPP;
+  constexpr int UNR = 4;
+  static_assert(PASSES % UNR == 0, "split/pass mismatch");
+  __shared__ float s_ml[TPP][G][2];
+  __shared__ float s_acc[TPP][G][D];
+
+  const int split = blockIdx.x, kh = blockIdx.y, b = blockIdx.z;
+  const int ctx = a.ctx[b];
+  const int t_begin = split * kDecodeSplit;
+  if (t_begin >= ctx) return;  // uniform across the workgroup
+  const int tid = threadIdx.x, tl = tid / LPT, c = tid % LPT;
+  const int h0 = kh * G;
+
+  float q[G][8];
+#pragma unroll
+  for (int gg = 0; gg < G; ++gg) {
+    const pack8 v = ld16(a.q + (int64_t)b * a.ldq + (h0 + gg) * D + c * 8);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      q[gg][2 * e] = lo_bf(v.w[e]);
+      q[gg][2 * e + 1] = hi_bf(v.w[e]);
+    }
+  }
+  float m[G], l[G], acc[G][8];
+#pragma unroll
+  for (int gg = 0; gg < G; ++gg) {
+    m[gg] = -INFINITY;
+    l[gg] = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[gg][e] = 0.f;
+  }
+
+  const int32_t* bt = a.block_table + (int64_t)b * a.max_blocks;
+  const int64_t kv_stride = (int64_t)a.n_kv_heads * 16 * D;  // K block -> V block
+  for (int p0 = 0; p0 < PASSES; p0 += UNR) {
+    pack8 kv[UNR], vv[UNR];
+    bool ok[UNR];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int tok = t_begin + (p0 + u) * TPP + tl;
+      ok[u] = tok < ctx;
+      kv[u] = zero8();
+      vv[u] = zero8();
+      if (ok[u]) {
+        const int phys = bt[tok >> 4];
+        const bf16_t* kp = a.pool + ((int64_t)phys * 2 * a.n_kv_heads + kh) * 16 * D +
+                           (tok & 15) * D + c * 8;
+        kv[u] = ld16(kp);
+        vv[u] = ld16(kp + kv_stride);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      float kf[8], vf[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        kf[2 * e] = lo_bf(kv[u].w[e]);
+        kf[2 * e + 1] = hi_bf(kv[u].w[e]);
+        vf[2 * e] = lo_bf(vv[u].w[e]);
+        vf[2 * e + 1] = hi_bf(vv[u].w[e]);
+      }
+#pragma unroll
+      for (int gg = 0; gg < G; ++gg) {
+        float sc = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sc += q[gg][e] * kf[e];
+#pragma unroll
+        for (int o = LPT / 2; o > 0; o >>= 1) sc += __shfl_xor(sc, o, 64);
+        if (ok[u]) {
+          const float s2 = sc * scale_log2;
+          const float mn = fmaxf(m[gg], s2);
+          const float corr = fast_exp2(m[gg] - mn);
+          const float pr = fast_exp2(s2 - mn);
+          m[gg] = mn;
+          l[gg] = l[gg] * corr + pr;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[gg][e] = acc[gg][e] * corr + pr * vf[e];
+        }
+      }
+    }
+  }
+
+#pragma unroll
+  for (int gg = 0; gg < G; ++gg) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s_acc[tl][gg][c * 8 + e] = acc[gg][e];
+    if (c == 0) {
+      s_ml[tl][gg][0] = m[gg];
+      s_ml[tl][gg][1] = l[gg];
+    }
+  }
+  __syncthreads();
+  for (int i = tid; i < G * D; i += 256) {
+    const int gg = i / D, d = i % D;
+    float M = -INFINITY;
+    for (int t = 0; t < TPP; ++t) M = fmaxf(M, s_ml[t][gg][0]);
+    float L = 0.f, O = 0.f;
+    for (int t = 0; t < TPP; ++t) {
+      const float mt = s_ml[t][gg][0];
+      if (mt == -INFINITY) continue;
+      const float w = fast_exp2(mt - M);
+      L += s_ml[t][gg][1] * w;
+      O += s_acc[t][gg][d] * w;
+    }
+    const int64_t idx = ((int64_t)b * a.n_heads + h0 + gg) * a.max_splits + split;
+    a.part_o[idx * D + d] = O;
+    if (d == 0) {
+      a.part_ml[idx * 2] = M;
+      a.part_ml[idx * 2 + 1] = L;
+    }
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(D) void attn_decode_combine_kernel(AttnDecodeArgs a) {
+  const int h = blockIdx.x, b = blockIdx.y, d = threadIdx.x;
+  const int n_splits = (a.ctx[b] + kDecodeSplit - 1) / kDecodeSplit;
+  const int64_t base = ((int64_t)b * a.n_heads + h) * a.max_splits;
+  float M = -INFINITY;
+  for (int sp = 0; sp < n_splits; ++sp) M = fmaxf(M, a.part_ml[(base + sp) * 2]);
+  float L = 0.f, O = 0.f;
+  for (int sp = 0; sp < n_splits; ++sp) {
+    const float w = fast_exp2(a.part_ml[(base + sp) * 2] - M);
+    L += a.part_ml[(base + sp) * 2 + 1] * w;
+    O += a.part_o[(base + sp) * D + d] * w;
+  }
+  a.out[(int64_t)b * a.ldo + h * D + d] = f2bf(O / L);
+}
+
+namespace {
+template <int D, int G>
+void launch_split(const AttnDecodeArgs& a, float sl, hipStream_t s) {
+  dim3 grid(a.call_splits, a.n_kv_heads, a.B);
+  hipLaunchKernelGGL((attn_decode_split_kernel<D, G>), grid, dim3(256), 0, s, a, sl);
+}
+template <int D>
+hipError_t launch_split_g(const AttnDecodeArgs& a, int G, float sl, hipStream_t s) {
+  switch (G) {
+    case 1: launch_split<D, 1>(a, sl, s); break;
+    case 2: launch_split<D, 2>(a, sl, s); break;
+    case 4: launch_split<D, 4>(a, sl, s); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+}  // namespace
+
+hipError_t attn_decode(const AttnDecodeArgs& a, hipStream_t s, LaunchInfo* info_split,
+                       LaunchInfo* info_combine) {
+  if (a.B <= 0) return hipSuccess;
+  if ((a.D != 64 && a.D != 128) || a.n_kv_heads <= 0 || a.n_heads % a.n_kv_heads) return hipErrorInvalidValue;
+  if (a.call_splits <= 0 || a.call_splits > a.max_splits || (a.ldq % 8)) return hipErrorInvalidValue;
+  const int G = a.n_heads / a.n_kv_heads;
+  const float sl = (float)(1.4426950408889634 / sqrt((double)a.D));
+  hipError_t e = a.D == 128 ? launch_split_g<128>(a, G, sl, s) : launch_split_g<64>(a, G, sl, s);
+  if (e != hipSuccess) return e;
+  dim3 grid(a.n_heads, a.B);
+  if (a.D == 128)
+    hipLaunchKernelGGL(attn_decode_combine_kernel<128>, grid, dim3(128), 0, s, a);
+  else
+    hipLaunchKernelGGL(attn_decode_combine_kernel<64>, grid, dim3(64), 0, s, a);
+  if (info_split) {
+    info_split->name = "attn_decode_split";
+    info_split->flops = 0;
+    info_split->bytes = a.kv_bytes;
+  }
+  if (info_combine) {
+    info_combine->name = "attn_decode_combine";
+    info_combine->flops = 0;
+    info_combine->bytes = 0;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace hs

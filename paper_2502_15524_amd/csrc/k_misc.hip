@@ -1,0 +1,221 @@
+// Memory-bound helpers of the stage forward pass: embedding gather, RMSNorm,
+// rotary embedding with paged KV append, greedy argmax and the KV block copy
+// used by export, import and merge.
+#include "hs_device.h"
+#include "hs_kernels.h"
+
+namespace hs {
+
+// ---------------------------------------------------------------- embedding
+
+__global__ __launch_bounds__(256) void embed_kernel(const int32_t* tok, const bf16_t* E, int vocab,
+                                                    int hidden, bf16_t* out) {
+  const int t = blockIdx.x;
+  const int id = tok[t];
+  const bool ok = id >= 0 && id < vocab;  // out-of-range ids give a zero row
+  const int chunks = hidden / 8;
+  for (int c = threadIdx.x; c < chunks; c += blockDim.x) {
+    const pack8 v = ok ? ld16(E + (int64_t)id * hidden + c * 8) : zero8();
+    st16(out + (int64_t)t * hidden + c * 8, v);
+  }
+}
+
+hipError_t embed(const int32_t* tok, const bf16_t* E, int vocab, int hidden, int n_tok,
+                 bf16_t* out, hipStream_t s, LaunchInfo* info) {
+  if (n_tok <= 0) return hipSuccess;
+  if (hidden % 8) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(embed_kernel, dim3(n_tok), dim3(256), 0, s, tok, E, vocab, hidden, out);
+  if (info) *info = LaunchInfo{"embed", 0, 4.0 * n_tok * (double)hidden};
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ RMSNorm
+
+// One workgroup per row; each thread keeps up to 4 chunks of 8 values.
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const bf16_t* x, int64_t ldx,
+                                                      const int32_t* rows, int hidden,
+                                                      const bf16_t* gain, float eps, bf16_t* out,
+                                                      int64_t ldo) {
+  __shared__ float red[4];
+  const int r = blockIdx.x;
+  const int src = rows ? rows[r] : r;
+  const bf16_t* xr = x + (int64_t)src * ldx;
+  const int chunks = hidden / 8;
+  float v[4][8];
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int c = threadIdx.x + i * 256;
+    if (c < chunks) {
+      const pack8 p = ld16(xr + c * 8);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[i][2 * e] = lo_bf(p.w[e]);
+        v[i][2 * e + 1] = hi_bf(p.w[e]);
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss += v[i][e] * v[i][e];
+    }
+  }
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float tot = red[0] + red[1] + red[2] + red[3];
+  const float inv = 1.0f / sqrtf(tot / (float)hidden + eps);
+  bf16_t* orow = out + (int64_t)r * ldo;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int c = threadIdx.x + i * 256;
+    if (c < chunks) {
+      const pack8 gp = ld16(gain + c * 8);
+      pack8 o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        o.w[e] = pack2bf(v[i][2 * e] * inv * lo_bf(gp.w[e]), v[i][2 * e + 1] * inv * hi_bf(gp.w[e]));
+      st16(orow + c * 8, o);
+    }
+  }
+}
+
+hipError_t rmsnorm(const bf16_t* x, int64_t ldx, const int32_t* rows, int n_rows, int hidden,
+                   const bf16_t* g, float eps, bf16_t* out, int64_t ldo, hipStream_t s,
+                   LaunchInfo* info) {
+  if (n_rows <= 0) return hipSuccess;
+  if ((hidden % 8) || hidden > 8192 || (ldx % 8) || (ldo % 8)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3(n_rows), dim3(256), 0, s, x, ldx, rows, hidden, g, eps,
+                     out, ldo);
+  if (info) *info = LaunchInfo{"rmsnorm", 0, 4.0 * n_rows * (double)hidden};
+  return hipGetLastError();
+}
+
+// --------------------------------------------------- RoPE + paged KV append
+//
+// One workgroup per token. q and k heads are rotated in place (rotate-half:
+// element i pairs with i + D/2, angle pos * base^(-2i/D) from the table);
+// the rotated k and the v of each KV head are written to the token's slot.
+
+__global__ __launch_bounds__(256) void rope_kv_kernel(RopeKvArgs a) {
+  const int t = blockIdx.x;
+  const int pos = a.pos[t];
+  const int slot = a.slot[t];
+  const int half = a.D / 2;
+  bf16_t* row = a.qkv + (int64_t)t * a.ld;
+  const float* ct = a.cos_t + (int64_t)pos * half;
+  const float* st = a.sin_t + (int64_t)pos * half;
+  const int64_t blk_base = slot >= 0 ? (int64_t)(slot >> 4) * 2 * a.n_kv_heads * 16 * a.D : 0;
+  const int off = slot & 15;
+  const int n_rot = (a.n_heads + a.n_kv_heads) * half;
+  for (int i = threadIdx.x; i < n_rot; i += blockDim.x) {
+    const int head = i / half, j = i % half;
+    bf16_t* hp = row + head * a.D;
+    const float x1 = bf2f(hp[j]), x2 = bf2f(hp[j + half]);
+    const float c = ct[j], sn = st[j];
+    const bf16_t y1 = f2bf(x1 * c - x2 * sn), y2 = f2bf(x2 * c + x1 * sn);
+    hp[j] = y1;
+    hp[j + half] = y2;
+    if (head >= a.n_heads && slot >= 0) {
+      bf16_t* kp = a.pool + blk_base + (int64_t)(head - a.n_heads) * 16 * a.D + off * a.D;
+      kp[j] = y1;
+      kp[j + half] = y2;
+    }
+  }
+  if (slot < 0) return;
+  const int vchunks = a.n_kv_heads * (a.D / 8);
+  for (int i = threadIdx.x; i < vchunks; i += blockDim.x) {
+    const int kh = i / (a.D / 8), c = i % (a.D / 8);
+    const pack8 v = ld16(row + (a.n_heads + a.n_kv_heads + kh) * a.D + c * 8);
+    st16(a.pool + blk_base + ((int64_t)a.n_kv_heads + kh) * 16 * a.D + off * a.D + c * 8, v);
+  }
+}
+
+hipError_t rope_kv(const RopeKvArgs& a, hipStream_t s, LaunchInfo* info) {
+  if (a.T <= 0) return hipSuccess;
+  if ((a.D % 16) || (a.ld % 8)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(rope_kv_kernel, dim3(a.T), dim3(256), 0, s, a);
+  if (info) {
+    const double row = (double)(a.n_heads + 2 * a.n_kv_heads) * a.D * 2;
+    *info = LaunchInfo{"rope_kv", 0, a.T * (row + (double)(a.n_heads + a.n_kv_heads) * a.D * 2 +
+                                            2.0 * a.n_kv_heads * a.D * 2)};
+  }
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------- argmax
+
+__device__ __forceinline__ void better(float& v, int& i, float v2, int i2) {
+  if (v2 > v || (v2 == v && i2 < i)) {
+    v = v2;
+    i = i2;
+  }
+}
+
+__global__ __launch_bounds__(256) void argmax_kernel(const float* logits, int n_cols, int32_t* out) {
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  const float* row = logits + (int64_t)blockIdx.x * n_cols;
+  float bv = -INFINITY;
+  int bi = 0x7FFFFFFF;
+  for (int c = threadIdx.x; c < n_cols; c += 256) better(bv, bi, row[c], c);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float v2 = __shfl_xor(bv, o, 64);
+    const int i2 = __shfl_xor(bi, o, 64);
+    better(bv, bi, v2, i2);
+  }
+  if ((threadIdx.x & 63) == 0) {
+    sv[threadIdx.x >> 6] = bv;
+    si[threadIdx.x >> 6] = bi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < 4; ++w) better(bv, bi, sv[w], si[w]);
+    out[blockIdx.x] = bi;
+  }
+}
+
+hipError_t argmax_rows(const float* logits, int n_rows, int n_cols, int32_t* out, hipStream_t s,
+                       LaunchInfo* info) {
+  if (n_rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(argmax_kernel, dim3(n_rows), dim3(256), 0, s, logits, n_cols, out);
+  if (info) *info = LaunchInfo{"argmax", 0, 4.0 * n_rows * (double)n_cols};
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ KV copy
+//
+// A unit is one KV block of one layer: the K block [n_kv][16][D] followed by
+// the V block, contiguous both in the pools and in the blob. Each workgroup
+// copies up to 16 KiB of one unit with 16-byte loads and stores.
+
+constexpr int kCopyBytesPerWg = 16384;
+
+__global__ __launch_bounds__(256) void kv_copy_kernel(const uint64_t* src, const uint64_t* dst,
+                                                      const int32_t* valid, int64_t unit_bytes,
+                                                      int D, int zero_tail) {
+  const int u = blockIdx.x;
+  const char* s = reinterpret_cast<const char*>(src[u]);
+  char* d = reinterpret_cast<char*>(dst[u]);
+  const int v = valid[u];
+  const int64_t begin = (int64_t)blockIdx.y * kCopyBytesPerWg;
+  const int64_t end = min(unit_bytes, begin + kCopyBytesPerWg);
+  const int64_t row_bytes = (int64_t)D * 2;
+  for (int64_t o = begin + threadIdx.x * 16; o < end; o += 256 * 16) {
+    const int slot = (int)((o / row_bytes) & 15);
+    pack8 x = zero8();
+    if (!zero_tail || slot < v) x = ld16(s + o);
+    st16(d + o, x);
+  }
+}
+
+hipError_t kv_copy(const uint64_t* src, const uint64_t* dst, const int32_t* valid, int n_units,
+                   int64_t unit_bytes, int D, int zero_tail, hipStream_t s, LaunchInfo* info) {
+  if (n_units <= 0) return hipSuccess;
+  if ((unit_bytes % 16) || (D % 8)) return hipErrorInvalidValue;
+  const int parts = (int)((unit_bytes + kCopyBytesPerWg - 1) / kCopyBytesPerWg);
+  hipLaunchKernelGGL(kv_copy_kernel, dim3(n_units, parts), dim3(256), 0, s, src, dst, valid,
+                     unit_bytes, D, zero_tail);
+  if (info) *info = LaunchInfo{"kv_copy", 0, 2.0 * n_units * (double)unit_bytes};
+  return hipGetLastError();
+}
+
+}  // namespace hs

@@ -1,0 +1,83 @@
+// Single-kernel entry points (include/hs_kernel.h).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "../../include/hs_kernel.h"
+#include "hs_host.h"
+#include "hs_kernels.h"
+
+using namespace hs;
+
+namespace {
+hs_status launched(hipError_t e, const char* what) {
+  if (e == hipErrorInvalidValue) return fail(HS_EINVAL, std::string(what) + ": unsupported shape");
+  if (e != hipSuccess) return fail(HS_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+  return HS_OK;
+}
+}  // namespace
+
+extern "C" hs_status hs_k_gemm(const void* X, int64_t ldx, const void* Wt, int64_t ldw, void* Y,
+                               int64_t ldy, const void* R, int64_t ldr, int32_t M, int32_t N,
+                               int32_t K, int32_t epi, void* stream) {
+  try {
+    if (!X || !Wt || !Y) return fail(HS_EINVAL, "null operand");
+    GemmArgs a{static_cast<const bf16_t*>(X), ldx, static_cast<const bf16_t*>(Wt), ldw, Y, ldy,
+               static_cast<const bf16_t*>(R), ldr, M, N, K};
+    return launched(gemm(a, epi, static_cast<hipStream_t>(stream), nullptr), "gemm");
+  } catch (...) {
+    return fail(HS_EINVAL, "unexpected internal error");
+  }
+}
+
+extern "C" hs_status hs_k_attn_prefill(const void* qkv, void* out, const int32_t* cu, int32_t n,
+                                       int32_t n_heads, int32_t n_kv_heads, int32_t head_dim,
+                                       void* stream) {
+  try {
+    if (!qkv || !out || !cu || n < 1) return fail(HS_EINVAL, "bad arguments");
+    if (n_kv_heads < 1 || n_heads % n_kv_heads) return fail(HS_EINVAL, "bad head counts");
+    if (cu[0] != 0) return fail(HS_EINVAL, "cu_seqlens[0] must be 0");
+    std::vector<int32_t> tiles;
+    for (int i = 0; i < n; ++i) {
+      const int len = cu[i + 1] - cu[i];
+      if (len < 1) return fail(HS_EINVAL, "sequence lengths must be >= 1");
+      for (int q = 0; q < len; q += 64) {
+        tiles.push_back(i);
+        tiles.push_back(q);
+      }
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    int32_t* d = nullptr;
+    const size_t nb = (size_t)(n + 1 + tiles.size()) * 4;
+    if (hipMalloc(reinterpret_cast<void**>(&d), nb) != hipSuccess)
+      return fail(HS_ENOMEM, "device allocation failed");
+    hipError_t e = hipMemcpy(d, cu, (n + 1) * 4, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(d + n + 1, tiles.data(), tiles.size() * 4, hipMemcpyHostToDevice);
+    const int ld = (n_heads + 2 * n_kv_heads) * head_dim;
+    AttnPrefillArgs a{static_cast<const bf16_t*>(qkv), ld, static_cast<bf16_t*>(out),
+                      n_heads * head_dim, d, d + n + 1, (int)(tiles.size() / 2), n_heads,
+                      n_kv_heads, head_dim, 0.0};
+    if (e == hipSuccess) e = attn_prefill(a, s, nullptr);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    (void)hipFree(d);
+    return launched(e, "attn_prefill");
+  } catch (...) {
+    return fail(HS_EINVAL, "unexpected internal error");
+  }
+}
+
+extern "C" hs_status hs_k_rmsnorm(const void* x, const void* g, void* out, int32_t rows,
+                                  int32_t hidden, float eps, void* stream) {
+  try {
+    if (!x || !g || !out || rows < 1) return fail(HS_EINVAL, "bad arguments");
+    return launched(rmsnorm(static_cast<const bf16_t*>(x), hidden, nullptr, rows, hidden,
+                            static_cast<const bf16_t*>(g), eps, static_cast<bf16_t*>(out), hidden,
+                            static_cast<hipStream_t>(stream), nullptr),
+                    "rmsnorm");
+  } catch (...) {
+    return fail(HS_EINVAL, "unexpected internal error");
+  }
+}

@@ -1,0 +1,128 @@
+"""Single-kernel parity on the GPU: GEMM epilogues, prefill attention and
+RMSNorm against float64 references of the same operation (the oracle's
+functions where it has them)."""
+import numpy as np
+import pytest
+
+from oracle.llama import attention, rms_norm, silu
+from workloads import gen
+from tests import gpu_util as G
+
+pytestmark = pytest.mark.gpu
+
+
+def _hs():
+    from paper_2502_15524_amd import hs
+    return hs
+
+
+GEMM_SHAPES = [(1, 256, 256), (7, 768, 256), (16, 1376, 256), (33, 512, 688),
+               (64, 4096, 4096), (65, 1024, 1024), (200, 768, 256), (512, 1024, 512),
+               (777, 1376, 688), (1024, 4096, 4096)]
+
+
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
+@pytest.mark.parametrize("epi", ["store", "resid", "swiglu", "f32"])
+def test_gemm(M, N, K, epi):
+    torch = G.torch()
+    hs = _hs()
+    rng = np.random.default_rng(M * 7 + N + K)
+    X = gen.round_to_bf16(rng.standard_normal((M, K)).astype(np.float32))
+    Wt = gen.round_to_bf16((rng.standard_normal((N, K)) * 0.05).astype(np.float32))
+    acc = X.astype(np.float64) @ Wt.astype(np.float64).T
+    dX, dW = G.to_dev_bf16(X), G.to_dev_bf16(Wt)
+    if epi == "f32":
+        Y = torch.zeros((M, N), dtype=torch.float32, device="cuda")
+        ref = acc
+    elif epi == "swiglu":
+        Y = torch.zeros((M, N // 2), dtype=torch.bfloat16, device="cuda")
+        idx = np.arange(N // 2)
+        gate = acc[:, (idx // 16) * 32 + idx % 16]
+        up = acc[:, (idx // 16) * 32 + 16 + idx % 16]
+        ref = silu(gate) * up
+    elif epi == "resid":
+        R = gen.round_to_bf16(rng.standard_normal((M, N)).astype(np.float32))
+        Y = G.to_dev_bf16(R)           # in place: Y = R + X W^T
+        ref = R + acc
+    else:
+        Y = torch.zeros((M, N), dtype=torch.bfloat16, device="cuda")
+        ref = acc
+    ldy = Y.shape[1]
+    hs.hs_k_gemm(dX.data_ptr(), K, dW.data_ptr(), K, Y.data_ptr(), ldy,
+                 Y.data_ptr() if epi == "resid" else 0, ldy, M, N, K, epi, G.stream_ptr())
+    torch.cuda.synchronize()
+    out = Y.cpu().numpy() if epi == "f32" else G.from_dev_bf16(Y)
+    scale = np.abs(ref).max()
+    err = np.abs(out - ref).max()
+    tol = (1e-5 if epi == "f32" else 8e-3) * scale
+    assert err <= tol, (err, scale)
+
+
+@pytest.mark.parametrize("lens,nh,nkv,d", [
+    ([1], 4, 4, 64), ([5, 64, 65], 4, 2, 64), ([130, 7, 300], 4, 4, 128),
+    ([257], 8, 2, 128), ([64, 128, 1, 33], 2, 1, 128)])
+def test_attn_prefill(lens, nh, nkv, d):
+    torch = G.torch()
+    hs = _hs()
+    rng = np.random.default_rng(sum(lens) + nh + d)
+    T = sum(lens)
+    qkv = gen.round_to_bf16((rng.standard_normal((T, (nh + 2 * nkv) * d)) * 1.5).astype(np.float32))
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    dq = G.to_dev_bf16(qkv)
+    out = torch.zeros((T, nh * d), dtype=torch.bfloat16, device="cuda")
+    hs.hs_k_attn_prefill(dq.data_ptr(), out.data_ptr(), list(cu), nh, nkv, d, G.stream_ptr())
+    torch.cuda.synchronize()
+    got = G.from_dev_bf16(out)
+    q = qkv[:, :nh * d].reshape(T, nh, d).astype(np.float64)
+    k = qkv[:, nh * d:(nh + nkv) * d].reshape(T, nkv, d).astype(np.float64)
+    v = qkv[:, (nh + nkv) * d:].reshape(T, nkv, d).astype(np.float64)
+    for i, n in enumerate(lens):
+        s = slice(cu[i], cu[i + 1])
+        ref = attention(q[s], k[s], v[s], np.arange(n), np.arange(n))
+        err = np.abs(got[s] - ref).max()
+        assert err <= 2e-2 * np.abs(ref).max() + 1e-3, (i, err)
+
+
+def test_attn_prefill_value_ones_gives_ones():
+    """V = 1 everywhere: every output is exactly a softmax row sum."""
+    torch = G.torch()
+    hs = _hs()
+    nh, nkv, d, lens = 4, 4, 128, [3, 100, 64]
+    T = sum(lens)
+    rng = np.random.default_rng(1)
+    qkv = np.ones((T, (nh + 2 * nkv) * d), np.float32)
+    qkv[:, :2 * nh * d] = rng.standard_normal((T, 2 * nh * d)) * 3
+    dq = G.to_dev_bf16(qkv)
+    out = torch.zeros((T, nh * d), dtype=torch.bfloat16, device="cuda")
+    hs.hs_k_attn_prefill(dq.data_ptr(), out.data_ptr(), [0, 3, 103, 167], nh, nkv, d,
+                         G.stream_ptr())
+    torch.cuda.synchronize()
+    got = G.from_dev_bf16(out)
+    assert np.max(np.abs(got - 1.0)) <= 2 ** -7
+
+
+@pytest.mark.parametrize("rows,hidden", [(1, 256), (37, 4096), (5, 5120), (3, 8192)])
+def test_rmsnorm(rows, hidden):
+    torch = G.torch()
+    hs = _hs()
+    rng = np.random.default_rng(rows + hidden)
+    x = gen.round_to_bf16((rng.standard_normal((rows, hidden)) * 3).astype(np.float32))
+    g = gen.round_to_bf16(rng.standard_normal(hidden).astype(np.float32))
+    dx, dg = G.to_dev_bf16(x), G.to_dev_bf16(g)
+    out = torch.zeros((rows, hidden), dtype=torch.bfloat16, device="cuda")
+    hs.hs_k_rmsnorm(dx.data_ptr(), dg.data_ptr(), out.data_ptr(), rows, hidden, 1e-5,
+                    G.stream_ptr())
+    torch.cuda.synchronize()
+    ref = rms_norm(x.astype(np.float64), g.astype(np.float64), 1e-5)
+    assert np.max(np.abs(G.from_dev_bf16(out) - ref)) <= 8e-3 * np.abs(ref).max()
+
+
+def test_gemm_rejects_unsupported_shapes():
+    torch = G.torch()
+    hs = _hs()
+    buf = torch.zeros(1 << 16, dtype=torch.bfloat16, device="cuda")
+    p = buf.data_ptr()
+    for (M, N, K, epi) in ((8, 24, 64, 0), (8, 64, 12, 0), (8, 48, 64, 2), (0, 64, 64, 0)):
+        with pytest.raises(hs.HSError) as e:
+            hs.hs_k_gemm(p, K, p, K, p, N, 0, 0, M, N, K, epi)
+        assert e.value.code == hs.HS_EINVAL

@@ -1,0 +1,345 @@
+"""End-to-end parity of the stage engine on the tiny workload (2 layers, two
+one-layer stages, 32-token prompt, 16 greedy decode steps), through the C ABI,
+against the CPU oracle; plus the bitwise invariants and the error paths."""
+import numpy as np
+import pytest
+
+import oracle
+from oracle import kvblob
+from oracle.llama import Stage as OStage, SyntheticWeights, greedy_generate
+from workloads import WORKLOADS, gen
+from tests import gpu_util as G
+
+pytestmark = pytest.mark.gpu
+
+WL = WORKLOADS["tiny-2x1"]
+CFG = WL.cfg
+LOGIT_TOL = 3e-2          # max |err| <= LOGIT_TOL * max |logit|
+
+
+@pytest.fixture(scope="module")
+def env():
+    from paper_2502_15524_amd import hs, pipeline
+    imgs = {}
+    for rb, re in ((0, 2), (0, 1), (1, 2)):
+        imgs[(rb, re)] = pipeline.pinned_image(CFG, rb, re)
+    W = SyntheticWeights(CFG)
+    prompt = gen.tokens(CFG.vocab, 32, WL.seed)
+    o_toks, o_logits = greedy_generate(CFG, W, prompt, WL.decode_steps, stages=list(WL.stages))
+    return dict(hs=hs, pipeline=pipeline, imgs=imgs, W=W, prompt=prompt, o_toks=o_toks,
+                o_logits=o_logits)
+
+
+def make(env, begin, end, resident=None, load=True, **kw):
+    rb, re = resident or (begin, end)
+    opts = dict(max_seqs=8, max_ctx=640, max_batch_tokens=1024)
+    opts.update(kw)
+    st = env["pipeline"].Stage(CFG, begin, end, resident=(rb, re), **opts)
+    if load:
+        st.load(env["imgs"][(rb, re)], chunk_bytes=1 << 18)
+    return st
+
+
+def run_greedy(stages, prompt, n_steps, seq_id=0):
+    """Prefill then greedy decode through stages in order; returns tokens and
+    the logits of every step (float32, host)."""
+    torch = G.torch()
+    sp = G.stream_ptr()
+    T = len(prompt)
+    x = torch.from_numpy(np.asarray(prompt, np.int32)).cuda()
+    nxt = torch.zeros(1, dtype=torch.int32, device="cuda")
+    logits = torch.zeros((1, CFG.vocab), dtype=torch.float32, device="cuda")
+    toks, lgs = [], []
+    for st in stages:
+        if st.end == CFG.n_layers:
+            st.prefill([seq_id], [T], x.data_ptr(), nxt.data_ptr(), logits.data_ptr(), sp)
+        else:
+            out = torch.zeros((T, CFG.hidden), dtype=torch.bfloat16, device="cuda")
+            st.prefill([seq_id], [T], x.data_ptr(), out.data_ptr(), 0, sp)
+            x = out
+    toks.append(int(nxt.item()))
+    lgs.append(logits.cpu().numpy()[0].copy())
+    for _ in range(n_steps):
+        x = nxt.clone()
+        for st in stages:
+            if st.end == CFG.n_layers:
+                st.decode([seq_id], x.data_ptr(), nxt.data_ptr(), logits.data_ptr(), sp)
+            else:
+                out = torch.zeros((1, CFG.hidden), dtype=torch.bfloat16, device="cuda")
+                st.decode([seq_id], x.data_ptr(), out.data_ptr(), 0, sp)
+                x = out
+        toks.append(int(nxt.item()))
+        lgs.append(logits.cpu().numpy()[0].copy())
+    return np.array(toks, np.int32), np.stack(lgs)
+
+
+def test_tiny_pipeline_matches_oracle(env):
+    s0, s1 = make(env, 0, 1), make(env, 1, 2)
+    toks, lgs = run_greedy([s0, s1], env["prompt"], WL.decode_steps)
+    ol = env["o_logits"]
+    err = np.abs(lgs - ol).max(axis=1) / np.abs(ol).max(axis=1)
+    srt = np.sort(ol, axis=1)
+    margin = (srt[:, -1] - srt[:, -2]) / np.abs(ol).max(axis=1)
+    print("per-step rel logit err", np.round(err, 4))
+    print("per-step oracle top-1/top-2 margin", np.round(margin, 4))
+    assert err.max() <= LOGIT_TOL
+    assert np.array_equal(toks, env["o_toks"]), (toks, env["o_toks"])
+
+
+def test_split_equals_full_bitwise(env):
+    s0, s1 = make(env, 0, 1), make(env, 1, 2)
+    t_pipe, l_pipe = run_greedy([s0, s1], env["prompt"], 6)
+    full = make(env, 0, 2)
+    t_full, l_full = run_greedy([full], env["prompt"], 6)
+    assert np.array_equal(t_pipe, t_full)
+    assert np.array_equal(l_pipe, l_full)
+
+
+def _hidden_prefill(st, tokens, seq_id=0):
+    torch = G.torch()
+    x = torch.from_numpy(np.asarray(tokens, np.int32)).cuda()
+    out = torch.zeros((len(tokens), CFG.hidden), dtype=torch.bfloat16, device="cuda")
+    st.prefill([seq_id], [len(tokens)], x.data_ptr(), out.data_ptr(), 0, G.stream_ptr())
+    return G.from_dev_bf16(out)
+
+
+def test_stage_boundary_hidden_matches_oracle(env):
+    st = make(env, 0, 1)
+    got = _hidden_prefill(st, env["prompt"])
+    ref = OStage(CFG, env["W"], 0, 1).prefill([0], [32], env["prompt"])
+    assert G.rel_fro(got, ref) <= 1e-2
+
+
+def test_causality_bitwise(env):
+    st = make(env, 0, 1)
+    t1 = gen.tokens(CFG.vocab, 100, 77)
+    t2 = t1.copy()
+    t2[70] = (t2[70] + 5) % CFG.vocab
+    h1 = _hidden_prefill(st, t1, seq_id=1)
+    h2 = _hidden_prefill(st, t2, seq_id=2)
+    assert np.array_equal(h1[:70], h2[:70])
+    assert not np.array_equal(h1[70], h2[70])
+
+
+def test_prefill_then_decode_close_to_recompute(env):
+    full = make(env, 0, 2)
+    toks, lgs = run_greedy([full], env["prompt"], 8, seq_id=3)
+    seq = np.concatenate([env["prompt"], toks[:-1]]).astype(np.int32)
+    fresh = make(env, 0, 2)
+    # logits of every extended position via prefills of growing prefixes
+    for k in (0, 4, 8):
+        n = len(env["prompt"]) + k
+        _, lf = run_greedy([fresh], seq[:n], 0, seq_id=100 + k)
+        assert np.abs(lf[0] - lgs[k]).max() <= LOGIT_TOL * np.abs(lgs[k]).max()
+
+
+def test_ragged_batch_prefill_and_decode(env):
+    """Several sequences in one call (ragged, some longer than one decode
+    split) against the oracle, sequence by sequence."""
+    torch = G.torch()
+    sp = G.stream_ptr()
+    lens = [1, 17, 300, 530]
+    ids = [11, 12, 13, 14]
+    prompts = [gen.tokens(CFG.vocab, n, 40 + i) for i, n in enumerate(lens)]
+    full = make(env, 0, 2)
+    x = torch.from_numpy(np.concatenate(prompts).astype(np.int32)).cuda()
+    nxt = torch.zeros(len(ids), dtype=torch.int32, device="cuda")
+    logits = torch.zeros((len(ids), CFG.vocab), dtype=torch.float32, device="cuda")
+    full.prefill(ids, lens, x.data_ptr(), nxt.data_ptr(), logits.data_ptr(), sp)
+    got = [logits.cpu().numpy().copy()]
+    for _ in range(3):
+        inp = nxt.clone()
+        full.decode(ids, inp.data_ptr(), nxt.data_ptr(), logits.data_ptr(), sp)
+        got.append(logits.cpu().numpy().copy())
+    # teacher-forced oracle on the engine's own tokens
+    for i, (sid, p) in enumerate(zip(ids, prompts)):
+        ost = OStage(CFG, env["W"], 0, 2)
+        ref = [ost.prefill([sid], [len(p)], p)[-1]]
+        cur = int(np.argmax(got[0][i]))
+        for step in range(3):
+            ref.append(ost.decode([sid], np.array([cur]))[0])
+            cur = int(np.argmax(got[step + 1][i]))
+        for step in range(4):
+            r = ref[step]
+            assert np.abs(got[step][i] - r).max() <= LOGIT_TOL * np.abs(r).max(), (sid, step)
+
+
+def _export(st, ids):
+    torch = G.torch()
+    hs = st_hs()
+    n = hs.hs_kv_export_size(st.h, ids)
+    buf = torch.zeros(n, dtype=torch.uint8, device="cuda")
+    w = hs.hs_kv_export(st.h, ids, buf.data_ptr(), n, G.stream_ptr())
+    assert w == n
+    return buf
+
+
+def st_hs():
+    from paper_2502_15524_amd import hs
+    return hs
+
+
+def test_kv_export_import_roundtrip_bitwise(env):
+    hs = env["hs"]
+    s0 = make(env, 0, 1)
+    _hidden_prefill(s0, env["prompt"], seq_id=5)
+    _hidden_prefill(s0, gen.tokens(CFG.vocab, 50, 9), seq_id=6)
+    blob = _export(s0, [6, 5])
+    b1 = blob.cpu().numpy().tobytes()
+    hdr, seqs = kvblob.parse(b1)          # the oracle's codec reads it
+    assert hdr["records"] == [(6, 50, 4), (5, 32, 2)]
+    # logical K/V content against the oracle's cache
+    ost = OStage(CFG, env["W"], 0, 1)
+    ost.prefill([5], [32], env["prompt"])
+    K, V = ost.kv[5][0]
+    k_gpu = gen.bf16_bits_to_f32(seqs[1][1][0])
+    v_gpu = gen.bf16_bits_to_f32(seqs[1][2][0])
+    assert np.abs(k_gpu - K).max() <= 2e-2 * np.abs(K).max()
+    assert np.abs(v_gpu - V).max() <= 2e-2 * np.abs(V).max()
+    # import into a fresh stage, export again: identical bytes
+    s0b = make(env, 0, 1)
+    hs.hs_kv_import(s0b.h, blob.data_ptr(), blob.numel(), G.stream_ptr())
+    assert hs.hs_seq_tokens(s0b.h, 5) == 32 and hs.hs_seq_tokens(s0b.h, 6) == 50
+    b2 = _export(s0b, [6, 5]).cpu().numpy().tobytes()
+    assert b1 == b2
+
+
+def test_import_then_continue_decoding_bitwise(env):
+    """Checkpoint/resume: a stage rebuilt from a blob decodes exactly like
+    the original."""
+    torch = G.torch()
+    hs = env["hs"]
+    full = make(env, 0, 2)
+    t_ref, l_ref = run_greedy([full], env["prompt"], 0, seq_id=7)
+    blob = _export(full, [7])
+    fresh = make(env, 0, 2)
+    hs.hs_kv_import(fresh.h, blob.data_ptr(), blob.numel(), G.stream_ptr())
+    sp = G.stream_ptr()
+    outs = []
+    for st in (full, fresh):
+        nxt = torch.tensor([int(t_ref[0])], dtype=torch.int32, device="cuda")
+        lg = torch.zeros((1, CFG.vocab), dtype=torch.float32, device="cuda")
+        seq = []
+        for _ in range(4):
+            inp = nxt.clone()
+            st.decode([7], inp.data_ptr(), nxt.data_ptr(), lg.data_ptr(), sp)
+            seq.append(lg.cpu().numpy().copy())
+        outs.append(np.stack(seq))
+    assert np.array_equal(outs[0], outs[1])
+
+
+def test_merge_equals_pipeline_bitwise(env):
+    hs = env["hs"]
+    a0, a1 = make(env, 0, 1), make(env, 1, 2)
+    b0, b1 = make(env, 0, 1), make(env, 1, 2)
+    ta, la = run_greedy([a0, a1], env["prompt"], 2, seq_id=1)
+    tb, lb = run_greedy([b0, b1], env["prompt"], 2, seq_id=1)
+    assert np.array_equal(la, lb)
+    merged = make(env, 0, 0, resident=(0, 2))
+    hs.hs_stage_merge(merged.h, [b0.h, b1.h], G.stream_ptr())
+    info = merged.info()
+    assert (info["layer_begin"], info["layer_end"]) == (0, 2) and info["live_seqs"] == 1
+    assert b0.info()["live_seqs"] == 0 and b1.info()["live_seqs"] == 0
+    # continue both from the same token
+    torch = G.torch()
+    sp = G.stream_ptr()
+    res = []
+    for stages in ([a0, a1], [merged]):
+        nxt = torch.tensor([int(ta[-1])], dtype=torch.int32, device="cuda")
+        lg = torch.zeros((1, CFG.vocab), dtype=torch.float32, device="cuda")
+        seq = []
+        for _ in range(5):
+            x = nxt.clone()
+            for st in stages:
+                if st.end == CFG.n_layers:
+                    st.decode([1], x.data_ptr(), nxt.data_ptr(), lg.data_ptr(), sp)
+                else:
+                    out = torch.zeros((1, CFG.hidden), dtype=torch.bfloat16, device="cuda")
+                    st.decode([1], x.data_ptr(), out.data_ptr(), 0, sp)
+                    x = out
+            seq.append(lg.cpu().numpy().copy())
+        res.append(np.stack(seq))
+    assert np.array_equal(res[0], res[1])
+
+
+def test_chunk_order_does_not_change_results(env):
+    torch = G.torch()
+    img = env["imgs"][(0, 2)]
+    ref_st = make(env, 0, 2)
+    _, l_ref = run_greedy([ref_st], env["prompt"], 2, seq_id=0)
+    st = make(env, 0, 2, load=False)
+    n_chunks = (img.numel() + (1 << 16) - 1) >> 16
+    order = np.random.default_rng(3).permutation(n_chunks)
+    st.load(img, chunk_bytes=1 << 16, order=list(order))
+    _, l = run_greedy([st], env["prompt"], 2, seq_id=0)
+    assert np.array_equal(l, l_ref)
+    assert env["hs"].hs_stage_loaded(st.h) == (2, img.numel())
+
+
+def test_error_paths(env):
+    torch = G.torch()
+    hs = env["hs"]
+    sp = G.stream_ptr()
+    x = torch.from_numpy(env["prompt"].astype(np.int32)).cuda()
+    out = torch.zeros((32, CFG.hidden), dtype=torch.bfloat16, device="cuda")
+
+    def code(f, *a):
+        with pytest.raises(hs.HSError) as e:
+            f(*a)
+        return e.value.code
+
+    st = make(env, 0, 1, load=False)
+    assert code(st.prefill, [0], [32], x.data_ptr(), out.data_ptr(), 0, sp) == hs.HS_ENOTREADY
+    img = env["imgs"][(0, 1)]
+    descs, _ = hs.hs_weight_layout(st.c, 0, 1)
+    layer0 = [d for d in descs if d["layer"] == 0]
+    # only the embedding and half of layer 0: still not ready
+    half = (layer0[0]["offset"] + layer0[-1]["offset"]) // 2
+    hs.hs_stage_load_chunk(st.h, 0, img.data_ptr(), half)
+    assert code(st.prefill, [0], [32], x.data_ptr(), out.data_ptr(), 0, sp) == hs.HS_ENOTREADY
+    assert st.info()["live_seqs"] == 0
+    # overlapping chunk rejected
+    assert code(hs.hs_stage_load_chunk, st.h, 256, img.data_ptr() + 256, 1024) == hs.HS_EINVAL
+    hs.hs_stage_load_chunk(st.h, half, img.data_ptr() + half, img.numel() - half)
+    st.prefill([0], [32], x.data_ptr(), out.data_ptr(), 0, sp)
+    # duplicate id, unknown id, too long
+    assert code(st.prefill, [0], [32], x.data_ptr(), out.data_ptr(), 0, sp) == hs.HS_EINVAL
+    one = torch.zeros(1, dtype=torch.int32, device="cuda")
+    o1 = torch.zeros((1, CFG.hidden), dtype=torch.bfloat16, device="cuda")
+    assert code(st.decode, [99], one.data_ptr(), o1.data_ptr(), 0, sp) == hs.HS_EINVAL
+    small = make(env, 0, 1, max_ctx=33)
+    small.prefill([0], [32], x.data_ptr(), out.data_ptr(), 0, sp)
+    small.decode([0], one.data_ptr(), o1.data_ptr(), 0, sp)
+    assert code(small.decode, [0], one.data_ptr(), o1.data_ptr(), 0, sp) == hs.HS_ERANGE
+    # export into a too-small buffer reports the size
+    need = hs.hs_kv_export_size(st.h, [0])
+    tiny = torch.zeros(64, dtype=torch.uint8, device="cuda")
+    with pytest.raises(hs.HSError) as e:
+        hs.hs_kv_export(st.h, [0], tiny.data_ptr(), 64, sp)
+    assert e.value.code == hs.HS_ERANGE and e.value.required == need
+    # host destination rejected
+    hbuf = torch.zeros(need, dtype=torch.uint8)
+    assert code(hs.hs_kv_export, st.h, [0], hbuf.data_ptr(), need, sp) == hs.HS_EINVAL
+    # corrupted blob leaves the target unchanged
+    blob = _export(st, [0])
+    tgt = make(env, 0, 1)
+    before = tgt.info()
+    bad = blob.clone()
+    bad[0] = 0
+    assert code(hs.hs_kv_import, tgt.h, bad.data_ptr(), bad.numel(), sp) == hs.HS_EINVAL
+    assert code(hs.hs_kv_import, tgt.h, blob.data_ptr(), blob.numel() - 16, sp) == hs.HS_EINVAL
+    assert tgt.info() == before
+    # blob layers not resident in the target
+    other = make(env, 1, 2)
+    assert code(hs.hs_kv_import, other.h, blob.data_ptr(), blob.numel(), sp) == hs.HS_EINVAL
+    # not enough blocks: nothing is written
+    cramped = make(env, 0, 1, kv_num_blocks=1)
+    assert code(hs.hs_kv_import, cramped.h, blob.data_ptr(), blob.numel(), sp) == hs.HS_ENOMEM
+    assert cramped.info()["live_seqs"] == 0 and cramped.info()["free_blocks"] == 1
+    # merge preconditions
+    m = make(env, 0, 0, resident=(0, 2))
+    s1 = make(env, 1, 2)
+    assert code(hs.hs_stage_merge, m.h, [st.h, s1.h], sp) == hs.HS_ESTATE  # different sequences
+    gap = make(env, 0, 0, resident=(0, 1))
+    assert code(hs.hs_stage_merge, gap.h, [st.h, s1.h], sp) == hs.HS_ESTATE  # not resident
+    assert st.info()["live_seqs"] == 1
