@@ -17,6 +17,10 @@
 #include "hs_device.h"
 #include "hs_kernels.h"
 
+#include <stdlib.h>
+
+#include <string>
+
 namespace hs {
 
 // ---------------------------------------------------------------- epilogue
@@ -137,6 +141,206 @@ __global__ __launch_bounds__(64 * (BN / WN) * (BM / WM)) void gemm_tiled(GemmArg
   }
 
   const int fq = (lane >> 4) * 4;
+#pragma unroll
+  for (int j = 0; j < TM; ++j) {
+    const int m = m0 + wm * WM + j * 16 + fr;
+    if constexpr (EPI == EPI_SWIGLU) {
+#pragma unroll
+      for (int i = 0; i < TN; i += 2)
+        store_swiglu(a, m, (n0 + wn * WN + i * 16) / 2 + fq, acc[i][j], acc[i + 1][j]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < TN; ++i) store4<EPI>(a, m, n0 + wn * WN + i * 16 + fq, acc[i][j]);
+    }
+  }
+}
+
+// ------------------------------------ tiled, buffer loads into an LDS ring
+//
+// Operand tiles go global -> LDS with buffer_load_dwordx4 ... lds (no register
+// staging): one instruction moves 64 lanes x 16 B of one operand into 1 KiB of
+// LDS, lane L landing at byte 16 L (8 rows x 64 k, or 16 rows x 32 k). The
+// buffer resource of each operand ends at its last row, so rows past M or N
+// read zeros and need no clamping; a lane's address is one 32-bit offset and
+// the per-instruction and per-k-step parts are scalar. LDS rows are unpadded;
+// the 16-byte chunks of a row are XOR-swizzled by the row index so the 16 rows
+// of an MFMA fragment read hit different banks. NS stages form a ring: the
+// loads for tile k + NS - 1 are in flight while tile k is multiplied, and a
+// wave waits only for tile k + 1 before the workgroup barrier. The copies are
+// issued from inline assembly so that the compiler neither tracks them nor
+// inserts waits for them; this code waits explicitly (vmcnt) before each
+// barrier. K must be a multiple of BK.
+
+typedef int v4i_t __attribute__((ext_vector_type(4)));
+
+constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, 32-bit data format
+
+__device__ __forceinline__ v4i_t buf_rsrc(const void* p, uint64_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(p);
+  const uint32_t n = bytes >= 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)bytes;
+  return v4i_t{(int)(uint32_t)a, (int)(uint32_t)((a >> 32) & 0xFFFFu), (int)n, kRsrcWord3};
+}
+
+// 64 lanes x 16 bytes from rsrc + voff + soff into LDS bytes [lds, lds + 1024)
+__device__ __forceinline__ void dma16(v4i_t rsrc, int voff, int soff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %3\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
+               :: "v"(voff), "s"(rsrc), "s"(soff), "s"(lds) : "memory");
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
+}
+
+__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+template <int BN, int BM, int BK, int NS>
+struct RTile {
+  static constexpr int CPR = BK / 8;           // 16-byte chunks per row
+  static constexpr int RPI = 64 / CPR;         // rows per load instruction
+  static constexpr int WN = BN / 2, WM = BM / 2, TN = WN / 16, TM = WM / 16;
+  static constexpr int WI = BN / 4 / RPI, XI = BM / 4 / RPI;  // instructions per wave
+  static constexpr int LPS = WI + XI;          // loads per stage per wave
+  static constexpr int W_BYTES = BN * BK * 2, STAGE = (BN + BM) * BK * 2;
+  static_assert(BK == 32 || BK == 64, "BK");
+  static_assert(WI >= 1 && XI >= 1, "tile too small for 4 waves");
+};
+
+// position of chunk c of row r inside its row
+template <int CPR>
+__device__ __forceinline__ int chunk_pos(int r, int c) {
+  if constexpr (CPR == 8) return c ^ (r & 7);
+  else return c ^ ((r >> 1) & 3);
+}
+
+// Multiply one stage (BK/32 steps of 32 k). Fragment reads are software
+// pipelined against the MFMAs and the order is pinned with scheduling group
+// barriers: the A fragment of row tile i+1 is read while the TM MFMAs of row
+// tile i run, and the B fragments of the next 32-k step are read during the
+// last row tile of the current one.
+template <int CPR>
+__device__ __forceinline__ bf16x8_v lds_frag(const bf16_t* s, int r, int c) {
+  return as_bf16x8(ld16(s + (r * CPR + chunk_pos<CPR>(r, c)) * 8));
+}
+
+template <int BN, int BM, int BK, int NS, int TN, int TM, typename Dma>
+__device__ __forceinline__ void ring_stage(f32x4_v (&acc)[TN][TM], const bf16_t* sw,
+                                           const bf16_t* sx, int wn, int wm, int fr, int g,
+                                           Dma&& dma) {
+  using T = RTile<BN, BM, BK, NS>;
+  constexpr int CPR = T::CPR, KS = BK / 32;
+  constexpr int MASK_MFMA = 0x008, MASK_DS_READ = 0x100;
+  bf16x8_v b[2][TM];
+  bf16x8_v a[2];
+#pragma unroll
+  for (int j = 0; j < TM; ++j) b[0][j] = lds_frag<CPR>(sx, wm * T::WM + j * 16 + fr, g);
+  a[0] = lds_frag<CPR>(sw, wn * T::WN + fr, g);
+  __builtin_amdgcn_sched_group_barrier(MASK_DS_READ, TM + 1, 0);
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    const int c = ks * 4 + g;
+#pragma unroll
+    for (int i = 0; i < TN; ++i) {
+      const int cur = i & 1, nxt = cur ^ 1;
+      dma(ks * TN + i);
+      if (i + 1 < TN) {
+        a[nxt] = lds_frag<CPR>(sw, wn * T::WN + (i + 1) * 16 + fr, c);
+      } else if (ks + 1 < KS) {
+#pragma unroll
+        for (int j = 0; j < TM; ++j)
+          b[(ks + 1) & 1][j] = lds_frag<CPR>(sx, wm * T::WM + j * 16 + fr, c + 4);
+        a[nxt] = lds_frag<CPR>(sw, wn * T::WN + fr, c + 4);
+      }
+#pragma unroll
+      for (int j = 0; j < TM; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[cur], b[ks & 1][j], acc[i][j], 0, 0, 0);
+      if (i + 1 < TN) __builtin_amdgcn_sched_group_barrier(MASK_DS_READ, 1, 0);
+      else if (ks + 1 < KS) __builtin_amdgcn_sched_group_barrier(MASK_DS_READ, TM + 1, 0);
+      __builtin_amdgcn_sched_group_barrier(MASK_MFMA, TM, 0);
+    }
+  }
+}
+
+template <int BN, int BM, int BK, int NS, int WPE, int SPREAD, int EPI>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
+void gemm_ring(GemmArgs a) {
+  using T = RTile<BN, BM, BK, NS>;
+  constexpr int CPR = T::CPR, RPI = T::RPI, WN = T::WN, WM = T::WM, TN = T::TN, TM = T::TM;
+  static_assert(EPI != EPI_SWIGLU || (WN % 32) == 0, "SwiGLU needs gate/up tile pairs");
+  __shared__ __attribute__((aligned(1024))) char smem[NS * T::STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wn = wave & 1, wm = wave >> 1;
+  const int tiles_m = (a.M + BM - 1) / BM;
+  int bid = blockIdx.x;
+  const int nb = gridDim.x;
+  if ((nb & 7) == 0) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
+  const int n0 = (bid / tiles_m) * BN, m0 = (bid % tiles_m) * BM;
+
+  const v4i_t rw = buf_rsrc(a.W, (uint64_t)a.N * a.ldw * 2);
+  const v4i_t rx = buf_rsrc(a.X, (uint64_t)a.M * a.ldx * 2);
+  const int lrow = lane / CPR;
+  const int lchunk = chunk_pos<CPR>(lrow, lane % CPR);  // row base is a multiple of RPI
+  const int vw = ((n0 + wave * (BN / 4) + lrow) * (int)a.ldw + lchunk * 8) * 2;
+  const int vx = ((m0 + wave * (BM / 4) + lrow) * (int)a.ldx + lchunk * 8) * 2;
+  const int sw_step = RPI * (int)a.ldw * 2, sx_step = RPI * (int)a.ldx * 2;
+  const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) char*)smem;
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  const uint32_t lds_w = lds0 + wave_s * (BN / 4) * BK * 2;
+  const uint32_t lds_x = lds0 + T::W_BYTES + wave_s * (BM / 4) * BK * 2;
+
+  // load instruction q of a stage: W rows first, then X rows
+  auto issue_one = [&](int stage, int kt, int q) {
+    const int kb = kt * BK * 2;
+    const uint32_t so = stage * T::STAGE;
+    if (q < T::WI) dma16(rw, vw, q * sw_step + kb, lds_w + so + q * 1024);
+    else dma16(rx, vx, (q - T::WI) * sx_step + kb, lds_x + so + (q - T::WI) * 1024);
+  };
+  auto issue = [&](int stage, int kt) {
+#pragma unroll
+    for (int q = 0; q < T::LPS; ++q) issue_one(stage, kt, q);
+  };
+  // spread the LPS loads of a stage over the TN * BK/32 row-tile steps
+  constexpr int STEPS = TN * (BK / 32);
+  auto issue_part = [&](int stage, int kt, int step) {
+#pragma unroll
+    for (int q = step * T::LPS / STEPS; q < (step + 1) * T::LPS / STEPS; ++q)
+      issue_one(stage, kt, q);
+  };
+
+  f32x4_v acc[TN][TM];
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+#pragma unroll
+    for (int j = 0; j < TM; ++j) acc[i][j] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+
+  const int fr = lane & 15, g = lane >> 4;
+  const int nk = a.K / BK;
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s)
+    if (s < nk) issue(s, s);
+  if (nk >= NS - 1) wait_vm<(NS - 2) * T::LPS>();
+  else wait_vm<0>();
+  wg_barrier();
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const int stage = kt % NS;
+    const bool more = kt + NS - 1 < nk;
+    const bf16_t* sw = reinterpret_cast<const bf16_t*>(smem + stage * T::STAGE);
+    const bf16_t* sx = reinterpret_cast<const bf16_t*>(smem + stage * T::STAGE + T::W_BYTES);
+    // SPREAD: the next stage's loads are issued between MFMA groups (best with
+    // one wave per SIMD); otherwise all at once before the stage's MFMAs.
+    if (!SPREAD && more) issue((kt + NS - 1) % NS, kt + NS - 1);
+    ring_stage<BN, BM, BK, NS>(acc, sw, sx, wn, wm, fr, g, [&](int step) {
+      if (SPREAD && more) issue_part((kt + NS - 1) % NS, kt + NS - 1, step);
+    });
+    if (more) wait_vm<(NS - 2) * T::LPS>();
+    else wait_vm<0>();
+    wg_barrier();
+  }
+
+  const int fq = g * 4;
 #pragma unroll
   for (int j = 0; j < TM; ++j) {
     const int m = m0 + wm * WM + j * 16 + fr;
@@ -282,6 +486,19 @@ hipError_t dispatch_epi_skinny(const GemmArgs& a, int epi, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <int BN, int BM, int BK, int NS, int WPE, int SPREAD>
+hipError_t dispatch_epi_ring(const GemmArgs& a, int epi, hipStream_t s) {
+  const int tiles = ((a.N + BN - 1) / BN) * ((a.M + BM - 1) / BM);
+  switch (epi) {
+    case EPI_STORE: hipLaunchKernelGGL((gemm_ring<BN, BM, BK, NS, WPE, SPREAD, EPI_STORE>), dim3(tiles), dim3(256), 0, s, a); break;
+    case EPI_RESID: hipLaunchKernelGGL((gemm_ring<BN, BM, BK, NS, WPE, SPREAD, EPI_RESID>), dim3(tiles), dim3(256), 0, s, a); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_ring<BN, BM, BK, NS, WPE, SPREAD, EPI_SWIGLU>), dim3(tiles), dim3(256), 0, s, a); break;
+    case EPI_F32: hipLaunchKernelGGL((gemm_ring<BN, BM, BK, NS, WPE, SPREAD, EPI_F32>), dim3(tiles), dim3(256), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 const char* kEpiName[4] = {"store", "resid", "swiglu", "f32"};
 
 }  // namespace
@@ -322,22 +539,35 @@ hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info) {
     }
     snprintf(name, sizeof name, "gemm_skinny_%s", kEpiName[epi]);
   } else {
+    // Tile choice; HS_GEMM_CFG forces one (tuning only).
+    static const char* force = getenv("HS_GEMM_CFG");
     const long t256 = (long)((a.N + 255) / 256) * ((a.M + 127) / 128);
     const long t128 = (long)((a.N + 127) / 128) * ((a.M + 127) / 128);
     const long t64 = (long)((a.N + 127) / 128) * ((a.M + 63) / 64);
-    if (t256 >= 256) {
-      e = dispatch_epi_tiled<256, 128, 64, 128, 64>(a, epi, s);
-      snprintf(name, sizeof name, "gemm_256x128_%s", kEpiName[epi]);
-    } else if (t128 >= 256) {
-      e = dispatch_epi_tiled<128, 128, 64, 64, 64>(a, epi, s);
-      snprintf(name, sizeof name, "gemm_128x128_%s", kEpiName[epi]);
-    } else if (t64 >= 128) {
-      e = dispatch_epi_tiled<128, 64, 64, 64, 32>(a, epi, s);
-      snprintf(name, sizeof name, "gemm_128x64_%s", kEpiName[epi]);
-    } else {
-      e = dispatch_epi_tiled<64, 64, 64, 32, 32>(a, epi, s);
-      snprintf(name, sizeof name, "gemm_64x64_%s", kEpiName[epi]);
-    }
+    const long b256 = (long)((a.N + 255) / 256) * ((a.M + 255) / 256);
+    // LDS-ring kernels: K % 64 == 0 and 32-bit byte offsets
+    const bool rok = (a.K % 64) == 0 && (uint64_t)a.N * a.ldw * 2 < (1ull << 31) &&
+                     (uint64_t)a.M * a.ldx * 2 < (1ull << 31);
+    const long r128 = (long)((a.N + 127) / 128) * ((a.M + 127) / 128);
+    std::string cfg;
+    if (force && *force) cfg = force;
+    else if (rok && b256 >= 256) cfg = "r256x256";       // large M: 1 wave / SIMD
+    else if (rok && r128 >= 384) cfg = "r128x128";       // 2 workgroups / CU
+    else if (rok) cfg = "r128x64";                       // few tiles: smaller ones
+    else if (t256 >= 256) cfg = "256x128";
+    else if (t128 >= 256) cfg = "128x128";
+    else if (t64 >= 128) cfg = "128x64";
+    else cfg = "64x64";
+    if (!rok && cfg[0] == 'r') cfg = "128x64";
+    if (cfg == "r256x256") e = dispatch_epi_ring<256, 256, 64, 2, 1, 1>(a, epi, s);
+    else if (cfg == "r256x128") e = dispatch_epi_ring<256, 128, 32, 3, 2, 0>(a, epi, s);
+    else if (cfg == "r128x128") e = dispatch_epi_ring<128, 128, 64, 2, 2, 0>(a, epi, s);
+    else if (cfg == "r128x64") e = dispatch_epi_ring<128, 64, 64, 3, 2, 0>(a, epi, s);
+    else if (cfg == "256x128") e = dispatch_epi_tiled<256, 128, 64, 128, 64>(a, epi, s);
+    else if (cfg == "128x128") e = dispatch_epi_tiled<128, 128, 64, 64, 64>(a, epi, s);
+    else if (cfg == "128x64") e = dispatch_epi_tiled<128, 64, 64, 64, 32>(a, epi, s);
+    else e = dispatch_epi_tiled<64, 64, 64, 32, 32>(a, epi, s);
+    snprintf(name, sizeof name, "gemm_%s_%s", cfg.c_str(), kEpiName[epi]);
   }
   if (info) {
     info->name = name;
