@@ -56,7 +56,8 @@ typedef enum {
  * RoPE (base), causal grouped-query attention with n_heads query heads over
  * n_kv_heads KV heads (query head h reads KV head h / (n_heads/n_kv_heads)),
  * SwiGLU FFN of width ffn, no biases, untied LM head. head_dim must be 64
- * or 128; hidden, ffn and n_heads*head_dim must be multiples of 16. */
+ * or 128, n_heads / n_kv_heads 1, 2 or 4; hidden a multiple of 64 (at most
+ * 8192), ffn and vocab multiples of 16. */
 typedef struct {
   int32_t n_layers, hidden, n_heads, n_kv_heads, head_dim, ffn, vocab;
   float rms_eps, rope_base;
@@ -81,11 +82,22 @@ typedef struct {
  *
  * The stage's weights are one packed byte image in a layout the library
  * defines (the counterpart of the prefetcher's shared-memory model file,
- * section 5.1). Every tensor is bf16, row-major [rows][cols], 256-byte
- * aligned, and the tensors of one layer are contiguous, so a layer is
- * usable as soon as one byte range has landed. Order: embedding (if the
- * resident range starts at layer 0), then each resident layer, then the
- * final norm and LM head (if it ends at the last layer).
+ * section 5.1). Every tensor is bf16 and 256-byte aligned, and the tensors of
+ * one layer are contiguous, so a layer is usable as soon as one byte range
+ * has landed. Order: embedding (if the resident range starts at layer 0),
+ * then each resident layer, then the final norm and LM head (if it ends at
+ * the last layer).
+ *
+ * Tiled matrices. The projection matrices (QKV, O, gate/up, down, LM head),
+ * logically [rows][cols] with cols the input dimension, are stored as 1 KiB
+ * blocks of 8 rows x 64 columns: with Kp = cols rounded up to 64, block
+ * (kb, nb) covers rows 8 nb .. 8 nb + 7 and columns 64 kb .. 64 kb + 63 and
+ * sits at byte offset (kb * rows / 8 + nb) * 1024 (column blocks outermost).
+ * Inside a block, row r (0..7) fills bytes [128 r, 128 r + 128), and its
+ * 16-byte chunk c (columns 64 kb + 8 c .. + 7) is stored at position c ^ r.
+ * Columns cols .. Kp - 1 are zero. A 64-column slab of any row range is then
+ * one contiguous run of bytes, in the order the GEMM kernels consume it.
+ * Embedding and norm gains are plain row-major.
  */
 typedef enum {
   HS_W_EMBED = 0,      /* [vocab][hidden] */
@@ -104,7 +116,9 @@ typedef struct {
   uint64_t offset, bytes; /* byte range inside the image */
   int32_t layer;          /* decoder layer; -1 for embedding, final norm, head */
   int32_t kind;           /* hs_weight_kind */
-  int64_t rows, cols;     /* stored shape */
+  int64_t rows, cols;     /* logical shape */
+  int32_t tiled;          /* 1: tiled matrix format (bytes = rows * Kp * 2) */
+  int32_t reserved;
 } hs_tensor_desc;
 
 /* Describe the image of resident layers [resident_begin, resident_end).
@@ -131,6 +145,11 @@ typedef enum {
 hs_status hs_image_put(const hs_model_cfg* cfg, int32_t resident_begin,
                        int32_t resident_end, int32_t layer, int32_t src_kind,
                        const uint16_t* src, uint64_t n_elems, void* image);
+
+/* Write a row-major bf16 matrix [rows][cols] (rows % 8 == 0) into the tiled
+ * matrix format at dst (rows * Kp * 2 bytes, host memory, caller-owned).
+ * Errors: HS_EINVAL for rows % 8 != 0 or a non-positive shape. */
+hs_status hs_pack_tiled(const uint16_t* src, int64_t rows, int64_t cols, void* dst);
 
 /* ------------------------------------------------------------------------
  * Stage lifecycle.

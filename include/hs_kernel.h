@@ -19,16 +19,18 @@
 extern "C" {
 #endif
 
-/* Y[m][n] = epilogue(sum_k X[m][k] W[n][k]) with fp32 accumulation; X, W bf16,
- * row-major with row strides ldx / ldw (elements). epi: 0 store bf16; 1 add
+/* Y[m][n] = epilogue(sum_k X[m][k] W[n][k]) with fp32 accumulation. X is
+ * bf16 row-major with row stride ldx (elements); W is the [N][K] matrix in
+ * the tiled matrix format of hs.h (hs_pack_tiled). epi: 0 store bf16; 1 add
  * the bf16 residual R (row stride ldr; may alias Y); 2 SwiGLU on gate/up rows
  * interleaved in groups of 16, Y has N/2 columns; 3 store float32. Requires
- * K % 8 == 0, N % 16 == 0 (N % 32 for SwiGLU), 16-byte aligned X, W, Y. This
- * is the projection arithmetic of every decoder layer (QKV, O, gate/up,
- * down) and of the LM head. */
-hs_status hs_k_gemm(const void* X, int64_t ldx, const void* W, int64_t ldw, void* Y,
-                    int64_t ldy, const void* R, int64_t ldr, int32_t M, int32_t N, int32_t K,
-                    int32_t epi, void* stream);
+ * K % 8 == 0, N % 16 == 0 (N % 32 for SwiGLU), 16-byte aligned X, W, Y; if
+ * K % 64 != 0, ldx must be at least K rounded up to 64 and the extra columns
+ * of X zero. This is the projection arithmetic of every decoder layer (QKV,
+ * O, gate/up, down) and of the LM head. */
+hs_status hs_k_gemm(const void* X, int64_t ldx, const void* W, void* Y, int64_t ldy,
+                    const void* R, int64_t ldr, int32_t M, int32_t N, int32_t K, int32_t epi,
+                    void* stream);
 
 /* Causal grouped-query attention over packed sequences (the attention of the
  * prefill pass). qkv: bf16 [T][(n_heads + 2 n_kv_heads) head_dim] holding

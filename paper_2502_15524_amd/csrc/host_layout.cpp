@@ -24,7 +24,7 @@ bool cfg_valid(const hs_model_cfg* c, std::string* why) {
   };
   if (!c) return no("null model cfg");
   if (c->n_layers <= 0) return no("n_layers must be positive");
-  if (c->hidden <= 0 || c->hidden % 16) return no("hidden must be a positive multiple of 16");
+  if (c->hidden <= 0 || c->hidden % 64) return no("hidden must be a positive multiple of 64");
   if (c->hidden > 8192) return no("hidden above 8192 is not supported");
   if (c->head_dim != 64 && c->head_dim != 128) return no("head_dim must be 64 or 128");
   if (c->n_heads <= 0 || c->n_kv_heads <= 0 || c->n_heads % c->n_kv_heads)
@@ -52,13 +52,17 @@ hs_status build_layout(const hs_model_cfg& c, int32_t rb, int32_t re, ImageLayou
   uint64_t off = 0;
   auto put = [&](int32_t layer, int32_t kind, uint64_t rows, uint64_t cols) {
     off = align_up(off, kAlign);
+    const bool tiled = !(kind == HS_W_EMBED || kind == HS_W_ATTN_NORM ||
+                         kind == HS_W_FFN_NORM || kind == HS_W_FINAL_NORM);
     hs_tensor_desc d;
     d.offset = off;
-    d.bytes = rows * cols * 2;
+    d.bytes = tiled ? tiled_bytes(rows, cols) : rows * cols * 2;
     d.layer = layer;
     d.kind = kind;
     d.rows = (int64_t)rows;
     d.cols = (int64_t)cols;
+    d.tiled = tiled ? 1 : 0;
+    d.reserved = 0;
     L->descs.push_back(d);
     off += d.bytes;
     return d.offset;
@@ -238,6 +242,14 @@ extern "C" hs_status hs_image_put(const hs_model_cfg* cfg, int32_t rb, int32_t r
       memcpy(img + dst_off, src, rows * cols * 2);
       return HS_OK;
     };
+    // n_rows source rows into a tiled matrix of `rows` rows, row i -> map(i)
+    auto tile = [&](uint64_t dst_off, uint64_t rows, uint64_t n_rows, uint64_t cols,
+                    auto map) -> hs_status {
+      if (n_elems != n_rows * cols) return fail(HS_EINVAL, "element count does not match the tensor shape");
+      tile_rows(src, n_rows, cols, rows, img + dst_off, map);
+      return HS_OK;
+    };
+    const uint64_t NQKV = QD + 2 * KD;
     switch (src_kind) {
       case HS_SRC_EMBED:
         if (!L.has_embed) return fail(HS_EINVAL, "image has no embedding");
@@ -247,29 +259,31 @@ extern "C" hs_status hs_image_put(const hs_model_cfg* cfg, int32_t rb, int32_t r
         return copy_rows(L.final_norm, 1, H);
       case HS_SRC_LM_HEAD:
         if (!L.has_head) return fail(HS_EINVAL, "image has no LM head");
-        return copy_rows(L.lm_head, V, H);
+        return tile(L.lm_head, V, V, H, [](uint64_t i) { return i; });
       case HS_SRC_ATTN_NORM: return copy_rows(ls->attn_norm, 1, H);
       case HS_SRC_FFN_NORM: return copy_rows(ls->ffn_norm, 1, H);
-      case HS_SRC_WQ: return copy_rows(ls->qkv, QD, H);
-      case HS_SRC_WK: return copy_rows(ls->qkv + QD * H * 2, KD, H);
-      case HS_SRC_WV: return copy_rows(ls->qkv + (QD + KD) * H * 2, KD, H);
-      case HS_SRC_WO: return copy_rows(ls->o, H, QD);
-      case HS_SRC_WDOWN: return copy_rows(ls->down, H, F);
+      case HS_SRC_WQ: return tile(ls->qkv, NQKV, QD, H, [](uint64_t i) { return i; });
+      case HS_SRC_WK: return tile(ls->qkv, NQKV, KD, H, [&](uint64_t i) { return QD + i; });
+      case HS_SRC_WV: return tile(ls->qkv, NQKV, KD, H, [&](uint64_t i) { return QD + KD + i; });
+      case HS_SRC_WO: return tile(ls->o, H, H, QD, [](uint64_t i) { return i; });
+      case HS_SRC_WDOWN: return tile(ls->down, H, H, F, [](uint64_t i) { return i; });
       case HS_SRC_WGATE:
-      case HS_SRC_WUP: {
-        if (n_elems != F * H) return fail(HS_EINVAL, "element count does not match the tensor shape");
-        const uint64_t up = src_kind == HS_SRC_WUP ? 16 : 0;
-        for (uint64_t f = 0; f < F; ++f) {
-          const uint64_t row = (f / 16) * 32 + up + (f % 16);
-          memcpy(img + ls->gateup + row * H * 2, src + f * H, H * 2);
-        }
-        return HS_OK;
-      }
+        return tile(ls->gateup, 2 * F, F, H, [](uint64_t f) { return (f / 16) * 32 + f % 16; });
+      case HS_SRC_WUP:
+        return tile(ls->gateup, 2 * F, F, H, [](uint64_t f) { return (f / 16) * 32 + 16 + f % 16; });
       default: return fail(HS_EINVAL, "unknown source tensor kind");
     }
   } catch (...) {
     return fail(HS_ENOMEM, "host allocation failed");
   }
+}
+
+extern "C" hs_status hs_pack_tiled(const uint16_t* src, int64_t rows, int64_t cols, void* dst) {
+  if (!src || !dst) return fail(HS_EINVAL, "null argument");
+  if (rows <= 0 || cols <= 0 || rows % 8) return fail(HS_EINVAL, "rows must be a positive multiple of 8");
+  tile_rows(src, (uint64_t)rows, (uint64_t)cols, (uint64_t)rows, static_cast<uint8_t*>(dst),
+            [](uint64_t i) { return i; });
+  return HS_OK;
 }
 
 extern "C" hs_status hs_kv_blob_describe(const void* host_blob, uint64_t avail,

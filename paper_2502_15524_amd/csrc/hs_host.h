@@ -40,6 +40,30 @@ struct ImageLayout {
 // Fails with HS_EINVAL on an invalid cfg or range.
 hs_status build_layout(const hs_model_cfg& cfg, int32_t rb, int32_t re, ImageLayout* out);
 
+// Tiled matrix format (see hs.h): byte offset of element (row, col) of a
+// matrix with `rows` rows, and its total size for `cols` columns.
+inline uint64_t round64(uint64_t x) { return (x + 63) / 64 * 64; }
+inline uint64_t tiled_bytes(uint64_t rows, uint64_t cols) { return rows * round64(cols) * 2; }
+inline uint64_t tiled_offset(uint64_t rows, uint64_t row, uint64_t col) {
+  const uint64_t kb = col / 64, nb = row / 8, r = row % 8, c = (col % 64) / 8;
+  return (kb * (rows / 8) + nb) * 1024 + r * 128 + ((c ^ r) * 16) + (col % 8) * 2;
+}
+// Copy row-major rows [0, n_rows) of src ([n_rows][cols]) into the tiled
+// matrix `dst` (total `rows` rows) at destination rows dst_row(i).
+template <typename RowMap>
+void tile_rows(const uint16_t* src, uint64_t n_rows, uint64_t cols, uint64_t rows, uint8_t* dst,
+               RowMap dst_row) {
+  for (uint64_t i = 0; i < n_rows; ++i) {
+    const uint64_t r = dst_row(i);
+    for (uint64_t c = 0; c < round64(cols); c += 8) {  // columns past cols are zero
+      const uint64_t n = c >= cols ? 0 : (cols - c < 8 ? cols - c : 8);
+      uint8_t* d = dst + tiled_offset(rows, r, c);
+      if (n) __builtin_memcpy(d, src + i * cols + c, n * 2);
+      if (n < 8) __builtin_memset(d + n * 2, 0, (8 - n) * 2);
+    }
+  }
+}
+
 // --------------------------------------------------------------- KV blob
 
 constexpr uint32_t kBlobVersion = 1;

@@ -20,7 +20,7 @@ enum Epi : int {
 
 struct GemmArgs {
   const bf16_t* X; int64_t ldx;  // [M][K] activations, row stride ldx elements
-  const bf16_t* W; int64_t ldw;  // [N][K] weights
+  const bf16_t* W;               // [N][K] weights in the tiled matrix format
   void* Y; int64_t ldy;          // output, row stride ldy elements (of its type)
   const bf16_t* R; int64_t ldr;  // residual input for EPI_RESID
   int M, N, K;
@@ -57,13 +57,17 @@ struct AttnPrefillArgs {
   const bf16_t* qkv; int64_t ld;  // post-RoPE q, k and v
   bf16_t* out; int64_t ldo;       // [T][n_heads * D]
   const int32_t* cu;              // [n_seqs + 1] token offsets
-  const int32_t* tiles;           // [n_tiles][2] (sequence, first query row)
+  const int32_t* tiles;           // [n_tiles][2] (sequence, first query row, multiple of q_tile)
   int n_tiles, n_heads, n_kv_heads, D;
+  int waves, q_tile;              // 4 or 8 waves; q_tile = 16 * waves queries per workgroup
   double flops;                   // unmasked-pair flops, for reporting
 };
 hipError_t attn_prefill(const AttnPrefillArgs& a, hipStream_t s, LaunchInfo* info);
+// Waves per prefill-attention workgroup for a problem with `tiles_of_128`
+// 128-query tiles (summed over sequences) and n_heads heads.
+int attn_prefill_waves(int64_t tiles_of_128, int n_heads);
 
-constexpr int kDecodeSplit = 256;  // tokens per split of the decode attention
+constexpr int kDecodeSplit = 64;   // tokens per split of the decode attention
 
 struct AttnDecodeArgs {
   const bf16_t* q; int64_t ldq;   // [B][ldq], query heads at column h * D

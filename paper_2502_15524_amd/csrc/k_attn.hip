@@ -3,7 +3,7 @@
 // Prefill reads post-RoPE q, k and v straight from the QKV GEMM output (the
 // whole prompt is in the call), one workgroup per (64-query tile, head).
 // Decode reads the paged KV pools through each sequence's block table; the
-// context is cut into fixed 256-token splits, so the split count depends on
+// context is cut into fixed 64-token splits, so the split count depends on
 // the context length only and the result is deterministic.
 #include "hs_device.h"
 #include "hs_kernels.h"
@@ -20,14 +20,19 @@ namespace hs {
 // (lane group g, element e -> key 4g+e for e<4, 16+4g+e-4 otherwise); V^T is
 // read from LDS with the same permutation, so the product is unchanged.
 
-template <int D>
-__global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefillArgs a, float scale_log2) {
+template <int D, int NW>
+__global__ __launch_bounds__(64 * NW) void attn_prefill_kernel(AttnPrefillArgs a, float scale_log2) {
+  constexpr int NT = 64 * NW;   // threads
+  constexpr int QT = 16 * NW;   // queries per workgroup
   constexpr int KB = 64;        // keys per block
   constexpr int LK = D + 8;     // padded K row in LDS
-  constexpr int LV = KB + 2;    // padded V^T row in LDS (33 dwords: conflict-free writes)
+  constexpr int LV = KB + 2;    // padded V^T row in LDS (33 dwords)
   constexpr int CPK = D / 8;    // 16-byte chunks per key row
+  constexpr int KPP = NT / CPK; // key rows per load pass
+  constexpr int PASS = KB / KPP;
+  static_assert(KB % KPP == 0 && (KPP % 2) == 0, "load mapping");
   __shared__ __attribute__((aligned(16))) bf16_t sK[KB * LK];
-  __shared__ __attribute__((aligned(16))) bf16_t sVt[D * LV];
+  __shared__ __attribute__((aligned(16))) uint32_t sVt[D * LV / 2];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int seq = a.tiles[2 * blockIdx.x], q0 = a.tiles[2 * blockIdx.x + 1];
@@ -36,7 +41,8 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefillArgs a, fl
   const int base = a.cu[seq], len = a.cu[seq + 1] - base;
   const int fr = lane & 15, g = lane >> 4;
 
-  const int qrow = q0 + wave * 16 + fr;  // this lane's query (position in sequence)
+  const int qw0 = q0 + wave * 16;        // first query of this wave
+  const int qrow = qw0 + fr;             // this lane's query (position in sequence)
   bf16x8_v qf[D / 32];
 #pragma unroll
   for (int ks = 0; ks < D / 32; ++ks) {
@@ -50,38 +56,51 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefillArgs a, fl
   for (int i = 0; i < D / 16; ++i) o[i] = f32x4_v{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
 
-  const int kend = min(len, q0 + 64);
+  const int kend = min(len, q0 + QT);
   const int n_kb = (kend + KB - 1) / KB;
   const bf16_t* kbase = a.qkv + (int64_t)base * a.ld + (a.n_heads + kh) * D;
   const bf16_t* vbase = a.qkv + (int64_t)base * a.ld + (a.n_heads + a.n_kv_heads + kh) * D;
+  const int lkey = tid / CPK, lcol = (tid % CPK) * 8;  // this thread's key row / column
+
+  pack8 kreg[PASS], vreg[PASS];
+  auto fetch = [&](int kb) {
+#pragma unroll
+    for (int p = 0; p < PASS; ++p) {
+      const int key = kb * KB + p * KPP + lkey;
+      kreg[p] = key < len ? ld16(kbase + (int64_t)key * a.ld + lcol) : zero8();
+      vreg[p] = key < len ? ld16(vbase + (int64_t)key * a.ld + lcol) : zero8();
+    }
+  };
+  fetch(0);
 
   for (int kb = 0; kb < n_kb; ++kb) {
     const int k0 = kb * KB;
-    __syncthreads();
-    // K block, row-major [key][d]
+    __syncthreads();  // every wave is done with the previous block
 #pragma unroll
-    for (int i = 0; i < KB * CPK / 256; ++i) {
-      const int c = tid + i * 256, key = c / CPK, col = (c % CPK) * 8;
-      pack8 v = zero8();
-      if (k0 + key < len) v = ld16(kbase + (int64_t)(k0 + key) * a.ld + col);
-      st16(&sK[key * LK + col], v);
-    }
-    // V block, transposed [d][key]; a wave covers 16 keys x 4 chunks
+    for (int p = 0; p < PASS; ++p) {
+      const int key = p * KPP + lkey;
+      st16(&sK[key * LK + lcol], kreg[p]);
+      // V^T: keys (2j, 2j+1) sit in lanes L and L ^ CPK; the even-key lane
+      // writes columns lcol..+3 and the odd-key lane lcol+4..+7, each as
+      // 4-byte (key pair) words.
+      uint32_t pw[4];
 #pragma unroll
-    for (int i = 0; i < KB * CPK / 256; ++i) {
-      const int c = tid + i * 256;
-      const int key = (c & 15) + 16 * (c / (16 * CPK)), col = ((c >> 4) % CPK) * 8;
-      pack8 v = zero8();
-      if (k0 + key < len) v = ld16(vbase + (int64_t)(k0 + key) * a.ld + col);
+      for (int e = 0; e < 4; ++e) pw[e] = __shfl_xor(vreg[p].w[e], CPK, 64);
+      const bool odd = key & 1;
+      const int kp = key >> 1;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        sVt[(col + 2 * e) * LV + key] = (bf16_t)(v.w[e] & 0xFFFFu);
-        sVt[(col + 2 * e + 1) * LV + key] = (bf16_t)(v.w[e] >> 16);
+      for (int e = 0; e < 2; ++e) {
+        const uint32_t mine = vreg[p].w[odd ? 2 + e : e], other = pw[odd ? 2 + e : e];
+        const uint32_t ev = odd ? other : mine, od = odd ? mine : other;  // even, odd key
+        const int col = lcol + (odd ? 4 : 0) + 2 * e;
+        sVt[(col) * (LV / 2) + kp] = (ev & 0xFFFFu) | (od << 16);
+        sVt[(col + 1) * (LV / 2) + kp] = (ev >> 16) | (od & 0xFFFF0000u);
       }
     }
     __syncthreads();
+    if (kb + 1 < n_kb) fetch(kb + 1);  // in flight during this block's MFMAs
+    if (k0 > qw0 + 15) continue;       // block entirely in this wave's future
 
-    // S^T for 4 subtiles of 16 keys
     f32x4_v s[4];
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
@@ -92,7 +111,6 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefillArgs a, fl
         s[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ks], s[t], 0, 0, 0);
       }
     }
-    // mask, scale, block max
     float bmax = -INFINITY;
 #pragma unroll
     for (int t = 0; t < 4; ++t)
@@ -106,7 +124,8 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefillArgs a, fl
       }
     bmax = fmaxf(bmax, __shfl_xor(bmax, 16, 64));
     bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
-    const float m_new = fmaxf(m_run, bmax);  // finite: key k0 <= every query of the tile
+    // finite: every wave processes block 0 and every query sees key 0
+    const float m_new = fmaxf(m_run, bmax);
     const float corr = fast_exp2(m_run - m_new);
     m_run = m_new;
     float psum = 0.f;
@@ -122,7 +141,6 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefillArgs a, fl
 #pragma unroll
     for (int i = 0; i < D / 16; ++i) o[i] *= corr;
 
-    // O^T += V^T P^T over two 32-key steps
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
       pack8 pb;
@@ -131,10 +149,10 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefillArgs a, fl
       pb.w[2] = pack2bf(s[2 * st + 1][0], s[2 * st + 1][1]);
       pb.w[3] = pack2bf(s[2 * st + 1][2], s[2 * st + 1][3]);
       const bf16x8_v pf = as_bf16x8(pb);
+      const int k1 = (st * 32 + g * 4) >> 1, k2 = (st * 32 + 16 + g * 4) >> 1;
 #pragma unroll
       for (int dt = 0; dt < D / 16; ++dt) {
-        const uint32_t* row = reinterpret_cast<const uint32_t*>(&sVt[(dt * 16 + fr) * LV]);
-        const int k1 = (st * 32 + g * 4) >> 1, k2 = (st * 32 + 16 + g * 4) >> 1;
+        const uint32_t* row = &sVt[(dt * 16 + fr) * (LV / 2)];
         pack8 vb;
         vb.w[0] = row[k1];
         vb.w[1] = row[k1 + 1];
@@ -162,19 +180,28 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefillArgs a, fl
 hipError_t attn_prefill(const AttnPrefillArgs& a, hipStream_t s, LaunchInfo* info) {
   if (a.n_tiles <= 0) return hipSuccess;
   if ((a.D != 64 && a.D != 128) || a.n_kv_heads <= 0 || a.n_heads % a.n_kv_heads) return hipErrorInvalidValue;
-  if ((a.ld % 8) || (a.ldo % 4)) return hipErrorInvalidValue;
+  if ((a.ld % 8) || (a.ldo % 4) || a.q_tile != 16 * a.waves || (a.waves != 4 && a.waves != 8))
+    return hipErrorInvalidValue;
   const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)a.D));
   dim3 grid(a.n_tiles, a.n_heads);
-  if (a.D == 128)
-    hipLaunchKernelGGL(attn_prefill_kernel<128>, grid, dim3(256), 0, s, a, scale_log2);
+  if (a.D == 128 && a.waves == 8)
+    hipLaunchKernelGGL((attn_prefill_kernel<128, 8>), grid, dim3(512), 0, s, a, scale_log2);
+  else if (a.D == 128)
+    hipLaunchKernelGGL((attn_prefill_kernel<128, 4>), grid, dim3(256), 0, s, a, scale_log2);
+  else if (a.waves == 8)
+    hipLaunchKernelGGL((attn_prefill_kernel<64, 8>), grid, dim3(512), 0, s, a, scale_log2);
   else
-    hipLaunchKernelGGL(attn_prefill_kernel<64>, grid, dim3(256), 0, s, a, scale_log2);
+    hipLaunchKernelGGL((attn_prefill_kernel<64, 4>), grid, dim3(256), 0, s, a, scale_log2);
   if (info) {
     info->name = a.D == 128 ? "attn_prefill_d128" : "attn_prefill_d64";
     info->flops = a.flops;
     info->bytes = 0;
   }
   return hipGetLastError();
+}
+
+int attn_prefill_waves(int64_t tiles_of_128, int n_heads) {
+  return tiles_of_128 * n_heads >= 512 ? 8 : 4;
 }
 
 // ------------------------------------------------------------------- decode
@@ -189,7 +216,7 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a
   constexpr int LPT = D / 8;        // lanes per token
   constexpr int TPP = 256 / LPT;    // tokens per pass
   constexpr int PASSES = kDecodeSplit / TPP;
-  constexpr int UNR = 4;
+  constexpr int UNR = PASSES < 4 ? PASSES : 4;
   static_assert(PASSES % UNR == 0, "split/pass mismatch");
   __shared__ float s_ml[TPP][G][2];
   __shared__ float s_acc[TPP][G][D];

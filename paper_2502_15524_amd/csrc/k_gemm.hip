@@ -8,9 +8,13 @@
 // 4 consecutive output features of one token and stores them as one 8-byte
 // write.
 //
+// The weight matrix W [N][K] is stored in the tiled matrix format (1 KiB
+// blocks of 8 rows x 64 k, chunk c of row r at position c ^ r, 64-column slabs
+// contiguous), so both kernels read weights in long contiguous runs.
+//
 // Two kernels:
-//  * gemm_tiled  - prefill: LDS double-buffered BN x BM x BK tiles, 4 waves,
-//                  16x16x32 bf16 MFMA, XCD-aware tile order.
+//  * gemm_ring   - prefill: BN x BM x 64 tiles copied straight into an LDS ring
+//                  of NS stages, 4 waves, 16x16x32 bf16 MFMA, XCD-aware order.
 //  * gemm_skinny - decode (M <= 64 tokens): HBM-bound weight streaming, 4
 //                  waves split K inside a workgroup, reduced through LDS in a
 //                  fixed order (deterministic).
@@ -55,121 +59,25 @@ __device__ __forceinline__ void store_swiglu(const GemmArgs& a, int m, int f, co
   *reinterpret_cast<uint2*>(static_cast<bf16_t*>(a.Y) + (int64_t)m * a.ldy + f) = o;
 }
 
-// ------------------------------------------------------------ tiled (prefill)
-
-template <int BN, int BM, int BK, int WN, int WM, int EPI>
-__global__ __launch_bounds__(64 * (BN / WN) * (BM / WM)) void gemm_tiled(GemmArgs a) {
-  constexpr int NWN = BN / WN, NWM = BM / WM, NT = 64 * NWN * NWM;
-  constexpr int TN = WN / 16, TM = WM / 16;
-  constexpr int LK = BK + 8;  // padded LDS row (elements)
-  constexpr int CPR = BK / 8; // 16-byte chunks per tile row
-  constexpr int WCH = BN * CPR / NT, XCH = BM * CPR / NT;
-  static_assert(BN * CPR % NT == 0 && BM * CPR % NT == 0, "tile/threads mismatch");
-  static_assert(EPI != EPI_SWIGLU || (WN % 32) == 0, "SwiGLU needs gate/up tile pairs");
-
-  __shared__ __attribute__((aligned(16))) bf16_t sW[2][BN * LK];
-  __shared__ __attribute__((aligned(16))) bf16_t sX[2][BM * LK];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wn = wave % NWN, wm = wave / NWN;
-
-  const int tiles_m = (a.M + BM - 1) / BM;
-  int bid = blockIdx.x;
-  const int nb = gridDim.x;
-  // Workgroups are dealt round-robin to the 8 XCDs; renumber so that each XCD
-  // gets a contiguous range of tiles (tiles sharing a weight panel share L2).
-  if ((nb & 7) == 0) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
-  const int n0 = (bid / tiles_m) * BN, m0 = (bid % tiles_m) * BM;
-
-  f32x4_v acc[TN][TM];
-#pragma unroll
-  for (int i = 0; i < TN; ++i)
-#pragma unroll
-    for (int j = 0; j < TM; ++j) acc[i][j] = f32x4_v{0.f, 0.f, 0.f, 0.f};
-
-  pack8 rw[WCH], rx[XCH];
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < WCH; ++i) {
-      const int c = tid + i * NT, row = c / CPR, k = k0 + (c % CPR) * 8, n = n0 + row;
-      rw[i] = (n < a.N && k < a.K) ? ld16(a.W + (int64_t)n * a.ldw + k) : zero8();
-    }
-#pragma unroll
-    for (int i = 0; i < XCH; ++i) {
-      const int c = tid + i * NT, row = c / CPR, k = k0 + (c % CPR) * 8, m = m0 + row;
-      rx[i] = (m < a.M && k < a.K) ? ld16(a.X + (int64_t)m * a.ldx + k) : zero8();
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < WCH; ++i) {
-      const int c = tid + i * NT;
-      st16(&sW[buf][(c / CPR) * LK + (c % CPR) * 8], rw[i]);
-    }
-#pragma unroll
-    for (int i = 0; i < XCH; ++i) {
-      const int c = tid + i * NT;
-      st16(&sX[buf][(c / CPR) * LK + (c % CPR) * 8], rx[i]);
-    }
-  };
-
-  const int nk = (a.K + BK - 1) / BK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  const int fr = lane & 15, kg = (lane >> 4) * 8;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * BK);
-    const bf16_t* ws = sW[cur] + (wn * WN + fr) * LK + kg;
-    const bf16_t* xs = sX[cur] + (wm * WM + fr) * LK + kg;
-#pragma unroll
-    for (int ks = 0; ks < BK / 32; ++ks) {
-      bf16x8_v af[TN], bf[TM];
-#pragma unroll
-      for (int i = 0; i < TN; ++i) af[i] = as_bf16x8(ld16(ws + i * 16 * LK + ks * 32));
-#pragma unroll
-      for (int j = 0; j < TM; ++j) bf[j] = as_bf16x8(ld16(xs + j * 16 * LK + ks * 32));
-#pragma unroll
-      for (int i = 0; i < TN; ++i)
-#pragma unroll
-        for (int j = 0; j < TM; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
-    }
-    if (kt + 1 < nk) sstore(cur ^ 1);
-    __syncthreads();
-  }
-
-  const int fq = (lane >> 4) * 4;
-#pragma unroll
-  for (int j = 0; j < TM; ++j) {
-    const int m = m0 + wm * WM + j * 16 + fr;
-    if constexpr (EPI == EPI_SWIGLU) {
-#pragma unroll
-      for (int i = 0; i < TN; i += 2)
-        store_swiglu(a, m, (n0 + wn * WN + i * 16) / 2 + fq, acc[i][j], acc[i + 1][j]);
-    } else {
-#pragma unroll
-      for (int i = 0; i < TN; ++i) store4<EPI>(a, m, n0 + wn * WN + i * 16 + fq, acc[i][j]);
-    }
-  }
-}
-
 // ------------------------------------ tiled, buffer loads into an LDS ring
 //
 // Operand tiles go global -> LDS with buffer_load_dwordx4 ... lds (no register
 // staging): one instruction moves 64 lanes x 16 B of one operand into 1 KiB of
-// LDS, lane L landing at byte 16 L (8 rows x 64 k, or 16 rows x 32 k). The
-// buffer resource of each operand ends at its last row, so rows past M or N
-// read zeros and need no clamping; a lane's address is one 32-bit offset and
-// the per-instruction and per-k-step parts are scalar. LDS rows are unpadded;
-// the 16-byte chunks of a row are XOR-swizzled by the row index so the 16 rows
-// of an MFMA fragment read hit different banks. NS stages form a ring: the
+// LDS, lane L landing at byte 16 L (8 rows x 64 k). A weight block of the
+// tiled format is exactly one such instruction (its chunks are already in the
+// LDS order), and consecutive row blocks of one 64-k slab are adjacent in
+// memory. Activations are row-major; the buffer resource ends at the last row,
+// so rows past M read zeros and need no clamping (weight rows past N only feed
+// outputs that are never stored). A lane's address is one 32-bit offset, the
+// per-instruction and per-k-step parts are scalar. LDS rows are unpadded; the
+// 16-byte chunks of a row are XOR-swizzled by the row index so the 16 rows of
+// an MFMA fragment read hit different banks. NS stages form a ring: the
 // loads for tile k + NS - 1 are in flight while tile k is multiplied, and a
 // wave waits only for tile k + 1 before the workgroup barrier. The copies are
 // issued from inline assembly so that the compiler neither tracks them nor
 // inserts waits for them; this code waits explicitly (vmcnt) before each
-// barrier. K must be a multiple of BK.
+// barrier. K is processed in 64-column slabs; when K % 64 != 0 the activation
+// columns up to the next multiple of 64 must be zero (the weights are).
 
 typedef int v4i_t __attribute__((ext_vector_type(4)));
 
@@ -184,7 +92,9 @@ __device__ __forceinline__ v4i_t buf_rsrc(const void* p, uint64_t bytes) {
 // 64 lanes x 16 bytes from rsrc + voff + soff into LDS bytes [lds, lds + 1024)
 __device__ __forceinline__ void dma16(v4i_t rsrc, int voff, int soff, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %3\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
-               :: "v"(voff), "s"(rsrc), "s"(soff), "s"(lds) : "memory");
+               :: "v"(voff), "s"(rsrc), "s"(__builtin_amdgcn_readfirstlane(soff)),
+                  "s"(__builtin_amdgcn_readfirstlane(lds))
+               : "memory");
 }
 
 template <int N>
@@ -203,7 +113,7 @@ struct RTile {
   static constexpr int WI = BN / 4 / RPI, XI = BM / 4 / RPI;  // instructions per wave
   static constexpr int LPS = WI + XI;          // loads per stage per wave
   static constexpr int W_BYTES = BN * BK * 2, STAGE = (BN + BM) * BK * 2;
-  static_assert(BK == 32 || BK == 64, "BK");
+  static_assert(BK == 64, "weights come in 64-column slabs");
   static_assert(WI >= 1 && XI >= 1, "tile too small for 4 waves");
 };
 
@@ -278,13 +188,18 @@ void gemm_ring(GemmArgs a) {
   if ((nb & 7) == 0) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
   const int n0 = (bid / tiles_m) * BN, m0 = (bid % tiles_m) * BM;
 
-  const v4i_t rw = buf_rsrc(a.W, (uint64_t)a.N * a.ldw * 2);
+  const int kp = (a.K + 63) & ~63;
+  const v4i_t rw = buf_rsrc(a.W, (uint64_t)a.N * kp * 2);
   const v4i_t rx = buf_rsrc(a.X, (uint64_t)a.M * a.ldx * 2);
   const int lrow = lane / CPR;
   const int lchunk = chunk_pos<CPR>(lrow, lane % CPR);  // row base is a multiple of RPI
-  const int vw = ((n0 + wave * (BN / 4) + lrow) * (int)a.ldw + lchunk * 8) * 2;
+  // weights: block (kt, n0/8 + wave * BN/32 + j) of the tiled format
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const int vw = lane * 16;
+  const int sw_base = (n0 / 8 + wave_u * (BN / 32)) * 1024, sw_step = 1024;
+  const int sw_slab = (a.N / 8) * 1024;
   const int vx = ((m0 + wave * (BM / 4) + lrow) * (int)a.ldx + lchunk * 8) * 2;
-  const int sw_step = RPI * (int)a.ldw * 2, sx_step = RPI * (int)a.ldx * 2;
+  const int sx_step = RPI * (int)a.ldx * 2;
   const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) char*)smem;
   const int wave_s = __builtin_amdgcn_readfirstlane(wave);
   const uint32_t lds_w = lds0 + wave_s * (BN / 4) * BK * 2;
@@ -292,10 +207,9 @@ void gemm_ring(GemmArgs a) {
 
   // load instruction q of a stage: W rows first, then X rows
   auto issue_one = [&](int stage, int kt, int q) {
-    const int kb = kt * BK * 2;
     const uint32_t so = stage * T::STAGE;
-    if (q < T::WI) dma16(rw, vw, q * sw_step + kb, lds_w + so + q * 1024);
-    else dma16(rx, vx, (q - T::WI) * sx_step + kb, lds_x + so + (q - T::WI) * 1024);
+    if (q < T::WI) dma16(rw, vw, sw_base + kt * sw_slab + q * sw_step, lds_w + so + q * 1024);
+    else dma16(rx, vx, (q - T::WI) * sx_step + kt * BK * 2, lds_x + so + (q - T::WI) * 1024);
   };
   auto issue = [&](int stage, int kt) {
 #pragma unroll
@@ -316,7 +230,7 @@ void gemm_ring(GemmArgs a) {
     for (int j = 0; j < TM; ++j) acc[i][j] = f32x4_v{0.f, 0.f, 0.f, 0.f};
 
   const int fr = lane & 15, g = lane >> 4;
-  const int nk = a.K / BK;
+  const int nk = kp / BK;
 #pragma unroll
   for (int s = 0; s < NS - 1; ++s)
     if (s < nk) issue(s, s);
@@ -356,22 +270,33 @@ void gemm_ring(GemmArgs a) {
 }
 
 // ------------------------------------------------------------ skinny (decode)
+//
+// A workgroup owns 16 * NF weight rows and all M <= 64 tokens; its 4 waves
+// split the 64-column slabs of K. For one slab, the rows' two (or four) 1 KiB
+// blocks are adjacent, so a wave reads 2 KiB per 16 rows contiguously; lane
+// (row fr, group g) takes chunk 4 ks + g of its row for the ks-th 32-k MFMA.
 
 template <int NF, int MCH, int U, int EPI>
 __global__ __launch_bounds__(256) void gemm_skinny(GemmArgs a) {
   static_assert(EPI != EPI_SWIGLU || (NF % 2) == 0, "SwiGLU needs gate/up tile pairs");
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n0 = blockIdx.x * 16 * NF;
-  const int kq = ((a.K + 127) / 128) * 32;  // per-wave K range, multiple of 32
-  const int kb = wave * kq, ke = min(a.K, kb + kq);
-  const int fr = lane & 15, kg = (lane >> 4) * 8;
+  const int kp = (a.K + 63) & ~63;
+  const int nslab = kp / 64;
+  const int sq = (nslab + 3) / 4;  // slabs per wave
+  const int sb = wave * sq, se = min(nslab, sb + sq);
+  const int fr = lane & 15, g = lane >> 4;
+  const int64_t slab_bytes = (int64_t)(a.N / 8) * 1024;
 
-  const bf16_t* wrow[NF];
+  const char* wrow[NF];
+  bool wok[NF];
 #pragma unroll
   for (int f = 0; f < NF; ++f) {
     const int n = n0 + 16 * f + fr;
-    wrow[f] = (n < a.N) ? a.W + (int64_t)n * a.ldw : nullptr;
+    wok[f] = n < a.N;
+    wrow[f] = reinterpret_cast<const char*>(a.W) + (int64_t)(n / 8) * 1024 + (n % 8) * 128;
   }
+  const int r8 = fr % 8;
   const bf16_t* xrow[MCH];
 #pragma unroll
   for (int c = 0; c < MCH; ++c) {
@@ -385,26 +310,35 @@ __global__ __launch_bounds__(256) void gemm_skinny(GemmArgs a) {
 #pragma unroll
     for (int c = 0; c < MCH; ++c) acc[f][c] = f32x4_v{0.f, 0.f, 0.f, 0.f};
 
-  for (int k0 = kb; k0 < ke; k0 += 32 * U) {
-    pack8 wv[NF][U], xv[MCH][U];
+  for (int s0 = sb; s0 < se; s0 += U) {
+    pack8 wv[NF][U][2], xv[MCH][U][2];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int k = k0 + 32 * u + kg;
-      const bool ok = k < ke;
+      const int sl = s0 + u;
+      const bool ok = sl < se;
 #pragma unroll
-      for (int f = 0; f < NF; ++f) wv[f][u] = (ok && wrow[f]) ? ld16(wrow[f] + k) : zero8();
+      for (int ks = 0; ks < 2; ++ks) {
+        const int chunk = ks * 4 + g;
 #pragma unroll
-      for (int c = 0; c < MCH; ++c) xv[c][u] = (ok && xrow[c]) ? ld16(xrow[c] + k) : zero8();
+        for (int f = 0; f < NF; ++f)
+          wv[f][u][ks] = (ok && wok[f])
+                             ? ld16(wrow[f] + sl * slab_bytes + ((chunk ^ r8) * 16))
+                             : zero8();
+#pragma unroll
+        for (int c = 0; c < MCH; ++c)
+          xv[c][u][ks] = (ok && xrow[c]) ? ld16(xrow[c] + sl * 64 + chunk * 8) : zero8();
+      }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int f = 0; f < NF; ++f)
+      for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-        for (int c = 0; c < MCH; ++c)
-          acc[f][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(wv[f][u]),
-                                                              as_bf16x8(xv[c][u]), acc[f][c],
-                                                              0, 0, 0);
+        for (int f = 0; f < NF; ++f)
+#pragma unroll
+          for (int c = 0; c < MCH; ++c)
+            acc[f][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                as_bf16x8(wv[f][u][ks]), as_bf16x8(xv[c][u][ks]), acc[f][c], 0, 0, 0);
   }
 
   __shared__ f32x4_v red[3][NF][MCH][64];
@@ -423,7 +357,7 @@ __global__ __launch_bounds__(256) void gemm_skinny(GemmArgs a) {
 #pragma unroll
       for (int c = 0; c < MCH; ++c) acc[f][c] += red[w][f][c][lane];
 
-  const int fq = (lane >> 4) * 4;
+  const int fq = g * 4;
 #pragma unroll
   for (int c = 0; c < MCH; ++c) {
     const int m = 16 * c + fr;
@@ -441,25 +375,6 @@ __global__ __launch_bounds__(256) void gemm_skinny(GemmArgs a) {
 // ------------------------------------------------------------------ launch
 
 namespace {
-
-template <int BN, int BM, int BK, int WN, int WM, int EPI>
-hipError_t launch_tiled(const GemmArgs& a, hipStream_t s) {
-  const int tiles = ((a.N + BN - 1) / BN) * ((a.M + BM - 1) / BM);
-  constexpr int NT = 64 * (BN / WN) * (BM / WM);
-  hipLaunchKernelGGL((gemm_tiled<BN, BM, BK, WN, WM, EPI>), dim3(tiles), dim3(NT), 0, s, a);
-  return hipGetLastError();
-}
-
-template <int BN, int BM, int BK, int WN, int WM>
-hipError_t dispatch_epi_tiled(const GemmArgs& a, int epi, hipStream_t s) {
-  switch (epi) {
-    case EPI_STORE: return launch_tiled<BN, BM, BK, WN, WM, EPI_STORE>(a, s);
-    case EPI_RESID: return launch_tiled<BN, BM, BK, WN, WM, EPI_RESID>(a, s);
-    case EPI_SWIGLU: return launch_tiled<BN, BM, BK, WN, WM, EPI_SWIGLU>(a, s);
-    case EPI_F32: return launch_tiled<BN, BM, BK, WN, WM, EPI_F32>(a, s);
-  }
-  return hipErrorInvalidValue;
-}
 
 template <int NF, int MCH, int U>
 hipError_t dispatch_epi_skinny(const GemmArgs& a, int epi, hipStream_t s) {
@@ -506,11 +421,15 @@ const char* kEpiName[4] = {"store", "resid", "swiglu", "f32"};
 hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info) {
   if (a.M <= 0 || a.N <= 0 || a.K <= 0) return hipErrorInvalidValue;
   if (epi < 0 || epi > 3) return hipErrorInvalidValue;
-  if ((a.K % 8) || (a.N % 16) || (a.ldx % 8) || (a.ldw % 8) || (a.ldy % 4)) return hipErrorInvalidValue;
+  const int64_t kp = (a.K + 63) / 64 * 64;
+  if ((a.K % 8) || (a.N % 16) || (a.ldx % 8) || (a.ldy % 4)) return hipErrorInvalidValue;
+  if ((a.K % 64) && a.ldx < kp) return hipErrorInvalidValue;
   if (epi == EPI_SWIGLU && (a.N % 32)) return hipErrorInvalidValue;
   if (epi == EPI_RESID && (!a.R || (a.ldr % 4))) return hipErrorInvalidValue;
-  if (((uintptr_t)a.X | (uintptr_t)a.W) & 15) return hipErrorInvalidValue;
-  if ((uintptr_t)a.Y & 15) return hipErrorInvalidValue;
+  if (((uintptr_t)a.X | (uintptr_t)a.W | (uintptr_t)a.Y) & 15) return hipErrorInvalidValue;
+  // 32-bit byte offsets in the buffer loads
+  if ((uint64_t)a.N * kp * 2 >= (1ull << 31) || (uint64_t)a.M * a.ldx * 2 >= (1ull << 31))
+    return hipErrorInvalidValue;
 
   static thread_local char name[64];
   const double flops = 2.0 * a.M * (double)a.N * a.K;
@@ -521,52 +440,37 @@ hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info) {
   hipError_t e;
   if (a.M <= 64) {
     const int mch = (a.M + 15) / 16;
-    const bool two = (epi == EPI_SWIGLU);
-    if (two) {
+    if (epi == EPI_SWIGLU) {
       switch (mch) {
-        case 1: e = dispatch_epi_skinny<2, 1, 4>(a, epi, s); break;
-        case 2: e = dispatch_epi_skinny<2, 2, 4>(a, epi, s); break;
-        case 3: e = dispatch_epi_skinny<2, 3, 2>(a, epi, s); break;
-        default: e = dispatch_epi_skinny<2, 4, 2>(a, epi, s); break;
+        case 1: e = dispatch_epi_skinny<2, 1, 2>(a, epi, s); break;
+        case 2: e = dispatch_epi_skinny<2, 2, 2>(a, epi, s); break;
+        case 3: e = dispatch_epi_skinny<2, 3, 1>(a, epi, s); break;
+        default: e = dispatch_epi_skinny<2, 4, 1>(a, epi, s); break;
       }
     } else {
       switch (mch) {
-        case 1: e = dispatch_epi_skinny<1, 1, 8>(a, epi, s); break;
-        case 2: e = dispatch_epi_skinny<1, 2, 4>(a, epi, s); break;
-        case 3: e = dispatch_epi_skinny<1, 3, 4>(a, epi, s); break;
-        default: e = dispatch_epi_skinny<1, 4, 2>(a, epi, s); break;
+        case 1: e = dispatch_epi_skinny<1, 1, 4>(a, epi, s); break;
+        case 2: e = dispatch_epi_skinny<1, 2, 2>(a, epi, s); break;
+        case 3: e = dispatch_epi_skinny<1, 3, 2>(a, epi, s); break;
+        default: e = dispatch_epi_skinny<1, 4, 1>(a, epi, s); break;
       }
     }
     snprintf(name, sizeof name, "gemm_skinny_%s", kEpiName[epi]);
   } else {
     // Tile choice; HS_GEMM_CFG forces one (tuning only).
     static const char* force = getenv("HS_GEMM_CFG");
-    const long t256 = (long)((a.N + 255) / 256) * ((a.M + 127) / 128);
-    const long t128 = (long)((a.N + 127) / 128) * ((a.M + 127) / 128);
-    const long t64 = (long)((a.N + 127) / 128) * ((a.M + 63) / 64);
     const long b256 = (long)((a.N + 255) / 256) * ((a.M + 255) / 256);
-    // LDS-ring kernels: K % 64 == 0 and 32-bit byte offsets
-    const bool rok = (a.K % 64) == 0 && (uint64_t)a.N * a.ldw * 2 < (1ull << 31) &&
-                     (uint64_t)a.M * a.ldx * 2 < (1ull << 31);
-    const long r128 = (long)((a.N + 127) / 128) * ((a.M + 127) / 128);
+    const long t256x128 = (long)((a.N + 255) / 256) * ((a.M + 127) / 128);
     std::string cfg;
     if (force && *force) cfg = force;
-    else if (rok && b256 >= 256) cfg = "r256x256";       // large M: 1 wave / SIMD
-    else if (rok && r128 >= 384) cfg = "r128x128";       // 2 workgroups / CU
-    else if (rok) cfg = "r128x64";                       // few tiles: smaller ones
-    else if (t256 >= 256) cfg = "256x128";
-    else if (t128 >= 256) cfg = "128x128";
-    else if (t64 >= 128) cfg = "128x64";
-    else cfg = "64x64";
-    if (!rok && cfg[0] == 'r') cfg = "128x64";
+    else if (b256 >= 256) cfg = "r256x256";       // large M: 1 wave / SIMD, 2 stages
+    else if (t256x128 >= 160) cfg = "r256x128s3"; // mid-size: 3-stage ring
+    else cfg = "r128x64s4";                       // few tiles: smaller ones, 4 stages
     if (cfg == "r256x256") e = dispatch_epi_ring<256, 256, 64, 2, 1, 1>(a, epi, s);
-    else if (cfg == "r256x128") e = dispatch_epi_ring<256, 128, 32, 3, 2, 0>(a, epi, s);
+    else if (cfg == "r256x128s3") e = dispatch_epi_ring<256, 128, 64, 3, 1, 1>(a, epi, s);
     else if (cfg == "r128x128") e = dispatch_epi_ring<128, 128, 64, 2, 2, 0>(a, epi, s);
     else if (cfg == "r128x64") e = dispatch_epi_ring<128, 64, 64, 3, 2, 0>(a, epi, s);
-    else if (cfg == "256x128") e = dispatch_epi_tiled<256, 128, 64, 128, 64>(a, epi, s);
-    else if (cfg == "128x128") e = dispatch_epi_tiled<128, 128, 64, 64, 64>(a, epi, s);
-    else if (cfg == "128x64") e = dispatch_epi_tiled<128, 64, 64, 64, 32>(a, epi, s);
-    else e = dispatch_epi_tiled<64, 64, 64, 32, 32>(a, epi, s);
+    else e = dispatch_epi_ring<128, 64, 64, 4, 1, 1>(a, epi, s);
     snprintf(name, sizeof name, "gemm_%s_%s", cfg.c_str(), kEpiName[epi]);
   }
   if (info) {

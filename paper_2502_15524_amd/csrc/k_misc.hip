@@ -90,48 +90,62 @@ hipError_t rmsnorm(const bf16_t* x, int64_t ldx, const int32_t* rows, int n_rows
 
 // --------------------------------------------------- RoPE + paged KV append
 //
-// One workgroup per token. q and k heads are rotated in place (rotate-half:
-// element i pairs with i + D/2, angle pos * base^(-2i/D) from the table);
-// the rotated k and the v of each KV head are written to the token's slot.
+// Work item = 4 consecutive rotation pairs (i, i + D/2), i = 4j .. 4j + 3, of
+// one q or k head of one token (8-byte loads and stores of each half), or one
+// 16-byte chunk of one v head. q and k are rotated in place (rotate-half,
+// angle pos * base^(-2i/D) from the table); the rotated k and the v of each
+// KV head are also written to the token's slot in the paged pool. Grid:
+// (tokens, work items / 256).
 
 __global__ __launch_bounds__(256) void rope_kv_kernel(RopeKvArgs a) {
   const int t = blockIdx.x;
+  const int half = a.D / 2, q4 = half / 4;          // 4-pair groups per head
+  const int n_rot = (a.n_heads + a.n_kv_heads) * q4;
+  const int n_v = a.n_kv_heads * (a.D / 8);
+  const int i = blockIdx.y * 256 + threadIdx.x;
+  if (i >= n_rot + n_v) return;
   const int pos = a.pos[t];
   const int slot = a.slot[t];
-  const int half = a.D / 2;
   bf16_t* row = a.qkv + (int64_t)t * a.ld;
-  const float* ct = a.cos_t + (int64_t)pos * half;
-  const float* st = a.sin_t + (int64_t)pos * half;
   const int64_t blk_base = slot >= 0 ? (int64_t)(slot >> 4) * 2 * a.n_kv_heads * 16 * a.D : 0;
   const int off = slot & 15;
-  const int n_rot = (a.n_heads + a.n_kv_heads) * half;
-  for (int i = threadIdx.x; i < n_rot; i += blockDim.x) {
-    const int head = i / half, j = i % half;
+  if (i < n_rot) {
+    const int head = i / q4, j = (i % q4) * 4;
     bf16_t* hp = row + head * a.D;
-    const float x1 = bf2f(hp[j]), x2 = bf2f(hp[j + half]);
-    const float c = ct[j], sn = st[j];
-    const bf16_t y1 = f2bf(x1 * c - x2 * sn), y2 = f2bf(x2 * c + x1 * sn);
-    hp[j] = y1;
-    hp[j + half] = y2;
+    const uint2 lo = *reinterpret_cast<const uint2*>(hp + j);
+    const uint2 hi = *reinterpret_cast<const uint2*>(hp + j + half);
+    const float4 c = *reinterpret_cast<const float4*>(a.cos_t + (int64_t)pos * half + j);
+    const float4 sn = *reinterpret_cast<const float4*>(a.sin_t + (int64_t)pos * half + j);
+    const float x1[4] = {lo_bf(lo.x), hi_bf(lo.x), lo_bf(lo.y), hi_bf(lo.y)};
+    const float x2[4] = {lo_bf(hi.x), hi_bf(hi.x), lo_bf(hi.y), hi_bf(hi.y)};
+    const float cc[4] = {c.x, c.y, c.z, c.w}, ss[4] = {sn.x, sn.y, sn.z, sn.w};
+    float y1[4], y2[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      y1[e] = x1[e] * cc[e] - x2[e] * ss[e];
+      y2[e] = x2[e] * cc[e] + x1[e] * ss[e];
+    }
+    const uint2 o1 = make_uint2(pack2bf(y1[0], y1[1]), pack2bf(y1[2], y1[3]));
+    const uint2 o2 = make_uint2(pack2bf(y2[0], y2[1]), pack2bf(y2[2], y2[3]));
+    *reinterpret_cast<uint2*>(hp + j) = o1;
+    *reinterpret_cast<uint2*>(hp + j + half) = o2;
     if (head >= a.n_heads && slot >= 0) {
       bf16_t* kp = a.pool + blk_base + (int64_t)(head - a.n_heads) * 16 * a.D + off * a.D;
-      kp[j] = y1;
-      kp[j + half] = y2;
+      *reinterpret_cast<uint2*>(kp + j) = o1;
+      *reinterpret_cast<uint2*>(kp + j + half) = o2;
     }
-  }
-  if (slot < 0) return;
-  const int vchunks = a.n_kv_heads * (a.D / 8);
-  for (int i = threadIdx.x; i < vchunks; i += blockDim.x) {
-    const int kh = i / (a.D / 8), c = i % (a.D / 8);
-    const pack8 v = ld16(row + (a.n_heads + a.n_kv_heads + kh) * a.D + c * 8);
-    st16(a.pool + blk_base + ((int64_t)a.n_kv_heads + kh) * 16 * a.D + off * a.D + c * 8, v);
+  } else if (slot >= 0) {
+    const int v = i - n_rot, kh = v / (a.D / 8), c = v % (a.D / 8);
+    const pack8 x = ld16(row + (a.n_heads + a.n_kv_heads + kh) * a.D + c * 8);
+    st16(a.pool + blk_base + ((int64_t)a.n_kv_heads + kh) * 16 * a.D + off * a.D + c * 8, x);
   }
 }
 
 hipError_t rope_kv(const RopeKvArgs& a, hipStream_t s, LaunchInfo* info) {
   if (a.T <= 0) return hipSuccess;
   if ((a.D % 16) || (a.ld % 8)) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(rope_kv_kernel, dim3(a.T), dim3(256), 0, s, a);
+  const int items = (a.n_heads + a.n_kv_heads) * (a.D / 8) + a.n_kv_heads * (a.D / 8);
+  hipLaunchKernelGGL(rope_kv_kernel, dim3(a.T, (items + 255) / 256), dim3(256), 0, s, a);
   if (info) {
     const double row = (double)(a.n_heads + 2 * a.n_kv_heads) * a.D * 2;
     *info = LaunchInfo{"rope_kv", 0, a.T * (row + (double)(a.n_heads + a.n_kv_heads) * a.D * 2 +

@@ -20,12 +20,12 @@ hs_status launched(hipError_t e, const char* what) {
 }
 }  // namespace
 
-extern "C" hs_status hs_k_gemm(const void* X, int64_t ldx, const void* Wt, int64_t ldw, void* Y,
-                               int64_t ldy, const void* R, int64_t ldr, int32_t M, int32_t N,
-                               int32_t K, int32_t epi, void* stream) {
+extern "C" hs_status hs_k_gemm(const void* X, int64_t ldx, const void* Wt, void* Y, int64_t ldy,
+                               const void* R, int64_t ldr, int32_t M, int32_t N, int32_t K,
+                               int32_t epi, void* stream) {
   try {
     if (!X || !Wt || !Y) return fail(HS_EINVAL, "null operand");
-    GemmArgs a{static_cast<const bf16_t*>(X), ldx, static_cast<const bf16_t*>(Wt), ldw, Y, ldy,
+    GemmArgs a{static_cast<const bf16_t*>(X), ldx, static_cast<const bf16_t*>(Wt), Y, ldy,
                static_cast<const bf16_t*>(R), ldr, M, N, K};
     return launched(gemm(a, epi, static_cast<hipStream_t>(stream), nullptr), "gemm");
   } catch (...) {
@@ -41,14 +41,18 @@ extern "C" hs_status hs_k_attn_prefill(const void* qkv, void* out, const int32_t
     if (n_kv_heads < 1 || n_heads % n_kv_heads) return fail(HS_EINVAL, "bad head counts");
     if (cu[0] != 0) return fail(HS_EINVAL, "cu_seqlens[0] must be 0");
     std::vector<int32_t> tiles;
+    int64_t tiles128 = 0;
     for (int i = 0; i < n; ++i) {
       const int len = cu[i + 1] - cu[i];
       if (len < 1) return fail(HS_EINVAL, "sequence lengths must be >= 1");
-      for (int q = 0; q < len; q += 64) {
+      tiles128 += (len + 127) / 128;
+    }
+    const int waves = attn_prefill_waves(tiles128, n_heads);
+    for (int i = 0; i < n; ++i)
+      for (int q = 0; q < cu[i + 1] - cu[i]; q += 16 * waves) {
         tiles.push_back(i);
         tiles.push_back(q);
       }
-    }
     hipStream_t s = static_cast<hipStream_t>(stream);
     int32_t* d = nullptr;
     const size_t nb = (size_t)(n + 1 + tiles.size()) * 4;
@@ -59,7 +63,7 @@ extern "C" hs_status hs_k_attn_prefill(const void* qkv, void* out, const int32_t
     const int ld = (n_heads + 2 * n_kv_heads) * head_dim;
     AttnPrefillArgs a{static_cast<const bf16_t*>(qkv), ld, static_cast<bf16_t*>(out),
                       n_heads * head_dim, d, d + n + 1, (int)(tiles.size() / 2), n_heads,
-                      n_kv_heads, head_dim, 0.0};
+                      n_kv_heads, head_dim, waves, 16 * waves, 0.0};
     if (e == hipSuccess) e = attn_prefill(a, s, nullptr);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     (void)hipFree(d);

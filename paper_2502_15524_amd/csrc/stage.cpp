@@ -344,7 +344,7 @@ struct LayerCall {
   int T;
   const int32_t *pos, *slot;             // device
   const int32_t *cu, *tiles;             // prefill
-  int n_tiles;
+  int n_tiles, attn_waves;
   double attn_flops;
   const int32_t *bt, *ctx;               // decode
   int call_splits;
@@ -355,6 +355,7 @@ hs_status layer_forward(hs_stage* st, int l, bf16_t* x, const LayerCall& c, hipS
   const hs_model_cfg& m = st->cfg;
   const LayerSlots& ls = st->L.layers[l - st->rb];
   const int H = m.hidden, D = m.head_dim, F = m.ffn;
+  const int FA = (int)round64(F);  // activation row stride: zero columns up to a multiple of 64
   const int NQKV = (m.n_heads + 2 * m.n_kv_heads) * D, QD = m.n_heads * D;
   hs_status r;
   r = run(st, s, [&](LaunchInfo* i) {
@@ -362,7 +363,7 @@ hs_status layer_forward(hs_stage* st, int l, bf16_t* x, const LayerCall& c, hipS
   });
   if (r != HS_OK) return r;
   r = run(st, s, [&](LaunchInfo* i) {
-    GemmArgs g{st->w_u, H, W(st, ls.qkv), H, st->w_qkv, NQKV, nullptr, 0, c.T, NQKV, H};
+    GemmArgs g{st->w_u, H, W(st, ls.qkv), st->w_qkv, NQKV, nullptr, 0, c.T, NQKV, H};
     return gemm(g, EPI_STORE, s, i);
   });
   if (r != HS_OK) return r;
@@ -375,7 +376,8 @@ hs_status layer_forward(hs_stage* st, int l, bf16_t* x, const LayerCall& c, hipS
   if (!c.decode) {
     r = run(st, s, [&](LaunchInfo* i) {
       AttnPrefillArgs a{st->w_qkv, NQKV, st->w_attn, QD, c.cu, c.tiles, c.n_tiles,
-                        m.n_heads, m.n_kv_heads, D, c.attn_flops};
+                        m.n_heads, m.n_kv_heads, D, c.attn_waves, 16 * c.attn_waves,
+                        c.attn_flops};
       return attn_prefill(a, s, i);
     });
   } else {
@@ -390,7 +392,7 @@ hs_status layer_forward(hs_stage* st, int l, bf16_t* x, const LayerCall& c, hipS
   }
   if (r != HS_OK) return r;
   r = run(st, s, [&](LaunchInfo* i) {
-    GemmArgs g{st->w_attn, QD, W(st, ls.o), QD, x, H, x, H, c.T, H, QD};
+    GemmArgs g{st->w_attn, QD, W(st, ls.o), x, H, x, H, c.T, H, QD};
     return gemm(g, EPI_RESID, s, i);
   });
   if (r != HS_OK) return r;
@@ -399,12 +401,12 @@ hs_status layer_forward(hs_stage* st, int l, bf16_t* x, const LayerCall& c, hipS
   });
   if (r != HS_OK) return r;
   r = run(st, s, [&](LaunchInfo* i) {
-    GemmArgs g{st->w_u, H, W(st, ls.gateup), H, st->w_act, F, nullptr, 0, c.T, 2 * F, H};
+    GemmArgs g{st->w_u, H, W(st, ls.gateup), st->w_act, FA, nullptr, 0, c.T, 2 * F, H};
     return gemm(g, EPI_SWIGLU, s, i);
   });
   if (r != HS_OK) return r;
   return run(st, s, [&](LaunchInfo* i) {
-    GemmArgs g{st->w_act, F, W(st, ls.down), F, x, H, x, H, c.T, H, F};
+    GemmArgs g{st->w_act, FA, W(st, ls.down), x, H, x, H, c.T, H, F};
     return gemm(g, EPI_RESID, s, i);
   });
 }
@@ -420,7 +422,7 @@ hs_status head_forward(hs_stage* st, const bf16_t* x, const int32_t* rows, int n
   if (r != HS_OK) return r;
   float* lg = logits ? logits : st->w_logits;
   r = run(st, s, [&](LaunchInfo* i) {
-    GemmArgs g{st->w_last, H, W(st, st->L.lm_head), H, lg, m.vocab, nullptr, 0, n, m.vocab, H};
+    GemmArgs g{st->w_last, H, W(st, st->L.lm_head), lg, m.vocab, nullptr, 0, n, m.vocab, H};
     return gemm(g, EPI_F32, s, i);
   });
   if (r != HS_OK) return r;
@@ -583,7 +585,7 @@ extern "C" hs_status hs_stage_create(const hs_model_cfg* cfg, int32_t layer_begi
   const uint64_t R = (uint64_t)st->ws_rows, S = (uint64_t)opts->max_seqs;
   uint64_t off = 0;
   std::vector<uint64_t> offs;
-  for (uint64_t sz : {R * H * 2, R * H * 2, R * NQKV * 2, R * QD * 2, R * F * 2, S * H * 2,
+  for (uint64_t sz : {R * H * 2, R * H * 2, R * NQKV * 2, R * QD * 2, R * round64(F) * 2, S * H * 2,
                       S * V * 4, S * m.n_heads * st->max_splits * (uint64_t)D * 4,
                       S * m.n_heads * st->max_splits * 2 * 4}) {
     offs.push_back(off);
@@ -591,6 +593,9 @@ extern "C" hs_status hs_stage_create(const hs_model_cfg* cfg, int32_t layer_begi
   }
   if (hipMalloc(reinterpret_cast<void**>(&st->d_ws), off) != hipSuccess)
     return bail(fail(HS_ENOMEM, "workspace allocation failed"));
+  // zero once: padding columns of the activations stay zero for good
+  if (hipMemset(st->d_ws, 0, off) != hipSuccess || hipDeviceSynchronize() != hipSuccess)
+    return bail(fail(HS_EHIP, "workspace initialisation failed"));
   st->w_x = reinterpret_cast<bf16_t*>(st->d_ws + offs[0]);
   st->w_u = reinterpret_cast<bf16_t*>(st->d_ws + offs[1]);
   st->w_qkv = reinterpret_cast<bf16_t*>(st->d_ws + offs[2]);
@@ -799,10 +804,16 @@ extern "C" hs_status hs_stage_prefill(hs_stage* st, int32_t n, const int64_t* id
       slot[cu[i] + p] = sq.blocks[p / kBlock] * kBlock + p % kBlock;
     }
     cu[i + 1] = cu[i] + lens[i];
-    for (int q = 0; q < lens[i]; q += 64) tiles.emplace_back(i, q);
     attn_flops += 4.0 * st->cfg.n_heads * st->cfg.head_dim * 0.5 * (double)lens[i] * (lens[i] + 1);
     st->seqs.emplace(ids[i], std::move(sq));
   }
+  // attention work tiles: q_tile queries of one sequence, longest rows first
+  int64_t tiles128 = 0;
+  for (int i = 0; i < n; ++i) tiles128 += (lens[i] + 127) / 128;
+  const int attn_waves = attn_prefill_waves(tiles128, st->cfg.n_heads);
+  const int q_tile = 16 * attn_waves;
+  for (int i = 0; i < n; ++i)
+    for (int q = 0; q < lens[i]; q += q_tile) tiles.emplace_back(i, q);
   std::stable_sort(tiles.begin(), tiles.end(),
                    [](const std::pair<int, int>& a, const std::pair<int, int>& b) {
                      return a.second > b.second;
@@ -841,6 +852,7 @@ extern "C" hs_status hs_stage_prefill(hs_stage* st, int32_t n, const int64_t* id
   c.cu = d_cu;
   c.tiles = d_tiles;
   c.n_tiles = (int)tiles.size();
+  c.attn_waves = attn_waves;
   c.attn_flops = attn_flops;
   for (int l = st->begin; l < st->end; ++l) {
     r = wait_need(s, nl[l - st->begin]);

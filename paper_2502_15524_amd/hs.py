@@ -47,7 +47,8 @@ class hs_stage_opts(C.Structure):
 
 class hs_tensor_desc(C.Structure):
     _fields_ = [("offset", C.c_uint64), ("bytes", C.c_uint64), ("layer", C.c_int32),
-                ("kind", C.c_int32), ("rows", C.c_int64), ("cols", C.c_int64)]
+                ("kind", C.c_int32), ("rows", C.c_int64), ("cols", C.c_int64),
+                ("tiled", C.c_int32), ("reserved", C.c_int32)]
 
 
 class hs_stage_info(C.Structure):
@@ -100,8 +101,9 @@ _SIGS = {
     "hs_stage_set_timing": [_P, C.c_int32],
     "hs_stage_read_timing": [_P, C.POINTER(hs_kernel_stat), C.c_int32, C.POINTER(C.c_int32)],
     # single-kernel entry points (include/hs_kernel.h)
-    "hs_k_gemm": [_P, C.c_int64, _P, C.c_int64, _P, C.c_int64, _P, C.c_int64, C.c_int32,
-                  C.c_int32, C.c_int32, C.c_int32, _P],
+    "hs_k_gemm": [_P, C.c_int64, _P, _P, C.c_int64, _P, C.c_int64, C.c_int32, C.c_int32,
+                  C.c_int32, C.c_int32, _P],
+    "hs_pack_tiled": [_P, C.c_int64, C.c_int64, _P],
     "hs_k_attn_prefill": [_P, _P, C.POINTER(C.c_int32), C.c_int32, C.c_int32, C.c_int32,
                           C.c_int32, _P],
     "hs_k_rmsnorm": [_P, _P, _P, C.c_int32, C.c_int32, C.c_float, _P],
@@ -171,7 +173,7 @@ def hs_weight_layout(cfg, resident_begin, resident_end):
     _check(lib().hs_weight_layout(C.byref(cfg), resident_begin, resident_end, arr, n.value,
                                   C.byref(n), C.byref(nbytes)))
     descs = [dict(offset=d.offset, bytes=d.bytes, layer=d.layer, kind=d.kind, rows=d.rows,
-                  cols=d.cols) for d in arr]
+                  cols=d.cols, tiled=d.tiled) for d in arr]
     return descs, nbytes.value
 
 
@@ -296,11 +298,15 @@ def hs_stage_read_timing(h, cap=256):
 EPI = {"store": 0, "resid": 1, "swiglu": 2, "f32": 3}
 
 
-def hs_k_gemm(X, ldx, W, ldw, Y, ldy, R, ldr, M, N, K, epi, stream=0):
+def hs_k_gemm(X, ldx, W, Y, ldy, R, ldr, M, N, K, epi, stream=0):
     if isinstance(epi, str):
         epi = EPI[epi]
-    _check(lib().hs_k_gemm(X, ldx, W, ldw, Y, ldy, R or None, ldr, M, N, K, epi,
-                           stream or None))
+    _check(lib().hs_k_gemm(X, ldx, W, Y, ldy, R or None, ldr, M, N, K, epi, stream or None))
+
+
+def hs_pack_tiled(src_ptr, rows, cols, dst_ptr):
+    """Row-major bf16 [rows][cols] at src_ptr -> tiled matrix format at dst_ptr."""
+    _check(lib().hs_pack_tiled(src_ptr, rows, cols, dst_ptr))
 
 
 def hs_k_attn_prefill(qkv, out, cu_seqlens, n_heads, n_kv_heads, head_dim, stream=0):

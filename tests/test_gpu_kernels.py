@@ -30,7 +30,12 @@ def test_gemm(M, N, K, epi):
     X = gen.round_to_bf16(rng.standard_normal((M, K)).astype(np.float32))
     Wt = gen.round_to_bf16((rng.standard_normal((N, K)) * 0.05).astype(np.float32))
     acc = X.astype(np.float64) @ Wt.astype(np.float64).T
-    dX, dW = G.to_dev_bf16(X), G.to_dev_bf16(Wt)
+    kp = -(-K // 64) * 64
+    Xp = np.zeros((M, kp), np.float32)     # columns past K are zero
+    Xp[:, :K] = X
+    dX = G.to_dev_bf16(Xp)
+    wt = G.tile_bits(gen.to_bf16_bits(Wt))
+    dW = torch.from_numpy(wt.view(np.int16)).cuda()
     if epi == "f32":
         Y = torch.zeros((M, N), dtype=torch.float32, device="cuda")
         ref = acc
@@ -48,7 +53,7 @@ def test_gemm(M, N, K, epi):
         Y = torch.zeros((M, N), dtype=torch.bfloat16, device="cuda")
         ref = acc
     ldy = Y.shape[1]
-    hs.hs_k_gemm(dX.data_ptr(), K, dW.data_ptr(), K, Y.data_ptr(), ldy,
+    hs.hs_k_gemm(dX.data_ptr(), kp, dW.data_ptr(), Y.data_ptr(), ldy,
                  Y.data_ptr() if epi == "resid" else 0, ldy, M, N, K, epi, G.stream_ptr())
     torch.cuda.synchronize()
     out = Y.cpu().numpy() if epi == "f32" else G.from_dev_bf16(Y)
@@ -60,7 +65,8 @@ def test_gemm(M, N, K, epi):
 
 @pytest.mark.parametrize("lens,nh,nkv,d", [
     ([1], 4, 4, 64), ([5, 64, 65], 4, 2, 64), ([130, 7, 300], 4, 4, 128),
-    ([257], 8, 2, 128), ([64, 128, 1, 33], 2, 1, 128)])
+    ([257], 8, 2, 128), ([64, 128, 1, 33], 2, 1, 128),
+    ([1024, 1024], 32, 8, 128)])     # enough 128-query tiles for the 8-wave variant
 def test_attn_prefill(lens, nh, nkv, d):
     torch = G.torch()
     hs = _hs()
@@ -122,7 +128,8 @@ def test_gemm_rejects_unsupported_shapes():
     hs = _hs()
     buf = torch.zeros(1 << 16, dtype=torch.bfloat16, device="cuda")
     p = buf.data_ptr()
-    for (M, N, K, epi) in ((8, 24, 64, 0), (8, 64, 12, 0), (8, 48, 64, 2), (0, 64, 64, 0)):
+    for (M, N, K, epi, ldx) in ((8, 24, 64, 0, 64), (8, 64, 12, 0, 64), (8, 48, 64, 2, 64),
+                                (0, 64, 64, 0, 64), (8, 64, 72, 0, 72)):
         with pytest.raises(hs.HSError) as e:
-            hs.hs_k_gemm(p, K, p, K, p, N, 0, 0, M, N, K, epi)
+            hs.hs_k_gemm(p, ldx, p, p, N, 0, 0, M, N, K, epi)
         assert e.value.code == hs.HS_EINVAL

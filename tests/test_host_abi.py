@@ -10,6 +10,7 @@ import oracle
 from oracle import kvblob
 from workloads import MODELS, gen
 from paper_2502_15524_amd import hs, pipeline
+from tests.gpu_util import tile_bits, untile_bits
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -30,23 +31,29 @@ def test_library_exports_every_declared_symbol():
     assert set(hs.EXPORTED) == declared
 
 
-@pytest.mark.parametrize("name", ["tiny", "llama2-7b", "llama2-13b", "llama3-8b"])
+@pytest.mark.parametrize("name", ["llama2-7b", "llama2-13b", "llama3-8b", "tiny"])
 def test_layout_matches_parameter_accounting(name):
     cfg = MODELS[name]
     c = pipeline.hs_cfg(cfg)
     descs, nbytes = hs.hs_weight_layout(c, 0, cfg.n_layers)
-    assert nbytes == oracle.image_bytes_16bit(cfg)
-    assert sum(d["bytes"] for d in descs) == oracle.image_bytes_16bit(cfg)
+    # tiled matrices pad their input dimension to a multiple of 64 (only the
+    # tiny model's FFN width 688 is not one)
+    pad = 0 if cfg.ffn % 64 == 0 else cfg.n_layers * cfg.hidden * (-cfg.ffn % 64) * 2
+    assert nbytes == oracle.image_bytes_16bit(cfg) + pad
+    assert sum(d["bytes"] for d in descs) == oracle.image_bytes_16bit(cfg) + pad
     prev_end = 0
     for d in descs:
         assert d["offset"] % 256 == 0 and d["offset"] >= prev_end
-        assert d["bytes"] == d["rows"] * d["cols"] * 2
+        kp = -(-d["cols"] // 64) * 64 if d["tiled"] else d["cols"]
+        assert d["bytes"] == d["rows"] * kp * 2
+        assert d["tiled"] == (d["kind"] in (hs.HS_W_QKV, hs.HS_W_O, hs.HS_W_GATEUP,
+                                            hs.HS_W_DOWN, hs.HS_W_LM_HEAD))
         prev_end = d["offset"] + d["bytes"]
     # stage cuts
     per = cfg.n_layers // 4 if cfg.n_layers % 4 == 0 else cfg.n_layers
     for b in range(0, cfg.n_layers, per):
         _, sb = hs.hs_weight_layout(c, b, b + per)
-        assert sb == oracle.image_bytes_16bit(cfg, b, b + per)
+        assert sb == oracle.image_bytes_16bit(cfg, b, b + per) + pad * per // cfg.n_layers
 
 
 def test_seven_b_middle_stage_image_bytes():
@@ -77,7 +84,10 @@ def test_image_put_places_tensors():
 
     def tensor(kind):
         d = by_kind[kind]
-        return u16[d["offset"] // 2:(d["offset"] + d["bytes"]) // 2].reshape(d["rows"], d["cols"])
+        raw = u16[d["offset"] // 2:(d["offset"] + d["bytes"]) // 2]
+        if d["tiled"]:
+            return untile_bits(raw, d["rows"], d["cols"])
+        return raw.reshape(d["rows"], d["cols"])
 
     qkv = tensor(hs.HS_W_QKV)
     wq = gen.to_bf16_bits(gen.weight_f32(cfg, 1, "wq"))
@@ -90,6 +100,10 @@ def test_image_put_places_tensors():
         assert np.array_equal(gu[(f // 16) * 32 + f % 16], g[f])
         assert np.array_equal(gu[(f // 16) * 32 + 16 + f % 16], u[f])
     assert np.all(tensor(hs.HS_W_ATTN_NORM) == 0x3F80)   # bf16 1.0
+    d = by_kind[hs.HS_W_DOWN]                             # 688 columns padded to 704
+    raw = u16[d["offset"] // 2:(d["offset"] + d["bytes"]) // 2]
+    wd = gen.to_bf16_bits(gen.weight_f32(cfg, 1, "wdown"))
+    assert np.array_equal(raw, tile_bits(wd))
     with pytest.raises(hs.HSError) as e:
         hs.hs_image_put(c, 1, 2, 0, "wq", wq.ctypes.data, wq.size, img.ctypes.data)
     assert e.value.code == hs.HS_EINVAL
@@ -153,3 +167,18 @@ def test_stage_create_validates_before_touching_the_gpu():
     with pytest.raises(hs.HSError) as e:
         hs.hs_weight_layout(bad, 0, 2)
     assert e.value.code == hs.HS_EINVAL
+
+
+def test_tiled_pack_matches_format_description():
+    """The library's packer agrees with the tiled format as documented."""
+    rng = np.random.default_rng(7)
+    bits = rng.integers(0, 65536, (24, 200), dtype=np.uint16)
+    dst = np.zeros(24 * 256, np.uint16)
+    hs.hs_pack_tiled(bits.ctypes.data, 24, 200, dst.ctypes.data)
+    assert np.array_equal(dst, tile_bits(bits))
+    # one element by hand: row 10, column 75 -> block (kb 1, nb 1), row 2, chunk 1
+    off = ((1 * 3 + 1) * 1024 + 2 * 128 + ((1 ^ 2) * 16) + 3 * 2) // 2
+    assert dst[off] == bits[10, 75]
+    assert np.all(untile_bits(dst, 24, 256)[:, 200:] == 0)
+    with pytest.raises(hs.HSError):
+        hs.hs_pack_tiled(bits.ctypes.data, 20, 200, dst.ctypes.data)
