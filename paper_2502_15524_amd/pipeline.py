@@ -59,11 +59,54 @@ def pack_image(cfg, rb, re, image_ptr, source=None, threads=8):
         list(ex.map(one, image_tensors(cfg, rb, re)))
 
 
+class PinnedBuffer:
+    """Page-locked host memory from hipHostMalloc, released on close() or
+    garbage collection (not cached). Exposes data_ptr() and numel() (bytes)."""
+
+    _hip = None
+
+    def __init__(self, nbytes):
+        import ctypes
+        if PinnedBuffer._hip is None:
+            lib = ctypes.CDLL("libamdhip64.so")
+            lib.hipHostMalloc.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_size_t,
+                                          ctypes.c_uint]
+            lib.hipHostMalloc.restype = ctypes.c_int
+            lib.hipHostFree.argtypes = [ctypes.c_void_p]
+            lib.hipHostFree.restype = ctypes.c_int
+            PinnedBuffer._hip = lib
+        self._p = ctypes.c_void_p()
+        rc = PinnedBuffer._hip.hipHostMalloc(ctypes.byref(self._p), nbytes, 0)
+        if rc != 0 or not self._p.value:
+            raise MemoryError(f"hipHostMalloc({nbytes}) failed with {rc}")
+        self._n = nbytes
+
+    def data_ptr(self):
+        return self._p.value
+
+    def numel(self):
+        return self._n
+
+    def numpy(self):
+        import ctypes
+        return np.ctypeslib.as_array((ctypes.c_uint8 * self._n).from_address(self._p.value))
+
+    def close(self):
+        if self._p is not None and self._p.value:
+            PinnedBuffer._hip.hipHostFree(self._p)
+            self._p = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
 def pinned_image(cfg, rb, re, source=None):
-    """A page-locked uint8 torch tensor holding the packed stage image."""
-    import torch
+    """A PinnedBuffer holding the packed image of resident layers [rb, re)."""
     _, nbytes = hs.hs_weight_layout(hs_cfg(cfg), rb, re)
-    img = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    img = PinnedBuffer(nbytes)
     pack_image(cfg, rb, re, img.data_ptr(), source)
     return img
 
