@@ -46,6 +46,9 @@ def parse():
     ap.add_argument("--chunk-mb", type=int, default=64)
     ap.add_argument("--copy-streams", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--traffic-probe", action="store_true",
+                    help="only run a few warm prefill steps and a 256 MiB device copy "
+                         "(the workload for hardware-counter passes)")
     return ap.parse_args()
 
 
@@ -137,6 +140,24 @@ def main():
         st.prefill([i], [P], x.data_ptr(), out.data_ptr(), 0, sp)
         return i
 
+    if args.traffic_probe:
+        # Counter passes read FETCH_SIZE / WRITE_SIZE per dispatch; the plain
+        # device-to-device copy of a known size calibrates them.
+        st.load(img, chunk)
+        st.sync()
+        for _ in range(3):
+            hs.hs_seq_free(st.h, prefill_once())
+        stream.synchronize()
+        src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+        dstc = torch.empty_like(src)
+        src.fill_(1)
+        for _ in range(2):
+            dstc.copy_(src)
+        torch.cuda.synchronize()
+        log("[bench] traffic probe done: 3 prefill steps, 2 copies of 268435456 bytes")
+        st.close()
+        return
+
     # ---------------------------------------------------------- cold TTFT
     cold, load_only = [], []
     for r in range(args.cold_runs + 1):
@@ -200,6 +221,19 @@ def main():
         bw = (s["bytes"] / s["launches"]) / (avg / 1e3) / 1e9 if s["bytes"] else 0
         log(f"[bench]   {s['name']:<28} x{s['launches'] // args.steps:<3} avg {avg * 1e3:8.1f} us "
             f"{100 * s['total_ms'] / kern_ms:5.1f}%  {rate:7.1f} TFLOP/s {bw:7.0f} GB/s")
+    # the same steps without per-kernel events (their cost inside the step)
+    ids = []
+    ev0.record(stream)
+    for _ in range(args.steps):
+        ids.append(prefill_once())
+        if len(ids) >= 3:
+            hs.hs_seq_free(st.h, ids.pop(0))
+    ev1.record(stream)
+    stream.synchronize()
+    for i in ids:
+        hs.hs_seq_free(st.h, i)
+    ms_step_plain = ev0.elapsed_time(ev1) / args.steps
+    log(f"[bench] same steps without kernel events: {ms_step_plain:.3f} ms/step")
     dom = max(stats, key=lambda s: s["total_ms"])
     dom_avg_s = dom["total_ms"] / dom["launches"] / 1e3
     dom_flops = dom["flops"] / dom["launches"]
@@ -272,6 +306,7 @@ def main():
                    "prompt_len": P, "weights": "N(0,0.02) bf16, seeded"},
         "roofline": roofline,
         "cpu_baseline": base,
+        "ms_per_step_without_kernel_events": round(ms_step_plain, 4),
         "prefill_mfma_frac_step": round(flops_step / t_prefill / 1e12 / PEAK_BF16_TFLOPS, 4),
         "cold_ttft_ms": round(t_cold * 1e3, 3),
         "cold_load_only_ms": round(t_load * 1e3, 3),

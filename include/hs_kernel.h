@@ -27,7 +27,12 @@ extern "C" {
  * K % 8 == 0, N % 16 == 0 (N % 32 for SwiGLU), 16-byte aligned X, W, Y; if
  * K % 64 != 0, ldx must be at least K rounded up to 64 and the extra columns
  * of X zero. This is the projection arithmetic of every decoder layer (QKV,
- * O, gate/up, down) and of the LM head. */
+ * O, gate/up, down) and of the LM head. Shapes with few output tiles split
+ * their k range over workgroups; the partial sums go through a workspace
+ * that the library allocates once per device (64 MiB + 256 KiB, on the first
+ * call) and keeps until the process ends, so calls on one device must not
+ * run concurrently. Results are deterministic: the same inputs give the same
+ * bits on every call. */
 hs_status hs_k_gemm(const void* X, int64_t ldx, const void* W, void* Y, int64_t ldy,
                     const void* R, int64_t ldr, int32_t M, int32_t N, int32_t K, int32_t epi,
                     void* stream);

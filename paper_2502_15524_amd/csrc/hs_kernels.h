@@ -24,6 +24,12 @@ struct GemmArgs {
   void* Y; int64_t ldy;          // output, row stride ldy elements (of its type)
   const bf16_t* R; int64_t ldr;  // residual input for EPI_RESID
   int M, N, K;
+  // Optional workspace for split-k tiles (stream-K launches): fp32 partial
+  // tiles and per-tile arrival counters, which must be zero before the first
+  // launch and are left at zero by every launch. Launches that share a
+  // workspace must not overlap in time.
+  float* part = nullptr; int64_t part_floats = 0;
+  uint32_t* flags = nullptr; int64_t flags_n = 0;
 };
 
 // Describes what was launched (for timing).

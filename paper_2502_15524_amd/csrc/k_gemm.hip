@@ -22,6 +22,9 @@
 #include "hs_kernels.h"
 
 #include <stdlib.h>
+#include <string.h>
+
+#include <algorithm>
 
 #include <string>
 
@@ -172,100 +175,235 @@ __device__ __forceinline__ void ring_stage(f32x4_v (&acc)[TN][TM], const bf16_t*
   }
 }
 
-template <int BN, int BM, int BK, int NS, int WPE, int SPREAD, int EPI>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
-void gemm_ring(GemmArgs a) {
+// Tile schedule. Output tiles are numbered in groups of `group_n` column
+// tiles (weight rows) by all row tiles (tokens), column tile fastest, so the
+// workgroups that run together on one XCD share weight and activation slabs
+// in its L2. A data-parallel launch runs one whole tile per workgroup. A
+// stream-K launch gives each of its G workgroups an equal contiguous share of
+// the (tile, 64-k step) iteration space; a tile whose k range is split
+// between workgroups is finished by whichever of them arrives last: every
+// contributor stores its fp32 partial tile, then bumps the tile's arrival
+// counter, and the one that completes the count adds the partials in k order
+// (so the result does not depend on the arrival order), applies the
+// epilogue and sets the counter back to zero. No workgroup waits for another.
+struct GemmSched {
+  int tiles_m, tiles_n, nk, group_n;
+  int sk;         // 1: stream-K over gridDim.x workgroups
+  int64_t total;  // tiles * nk
+};
+
+__device__ __forceinline__ void tile_coords(const GemmSched& s, int t, int& nt, int& mt) {
+  const int per = s.group_n * s.tiles_m;
+  const int gi = t / per, r = t - gi * per;
+  const int first = gi * s.group_n;
+  const int gsz = min(s.tiles_n - first, s.group_n);
+  nt = first + r % gsz;
+  mt = r / gsz;
+}
+
+// Stream-K: workgroup g owns iterations [floor(g T / G), floor((g+1) T / G)).
+__device__ __forceinline__ int64_t sk_begin(int g, int64_t total, int G) {
+  return (int64_t)g * total / G;
+}
+__device__ __forceinline__ int sk_owner(int64_t i, int64_t total, int G) {
+  return (int)(((i + 1) * G - 1) / total);
+}
+
+template <int BN, int BM, int NS, int SPR, bool SK, int EPI>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void gemm_ring(GemmArgs a, GemmSched sc) {
+  constexpr int BK = 64;
   using T = RTile<BN, BM, BK, NS>;
   constexpr int CPR = T::CPR, RPI = T::RPI, WN = T::WN, WM = T::WM, TN = T::TN, TM = T::TM;
+  constexpr int LPS = T::LPS;
   static_assert(EPI != EPI_SWIGLU || (WN % 32) == 0, "SwiGLU needs gate/up tile pairs");
   __shared__ __attribute__((aligned(1024))) char smem[NS * T::STAGE];
+  __shared__ int s_last;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wn = wave & 1, wm = wave >> 1;
-  const int tiles_m = (a.M + BM - 1) / BM;
-  int bid = blockIdx.x;
-  const int nb = gridDim.x;
-  if ((nb & 7) == 0) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
-  const int n0 = (bid / tiles_m) * BN, m0 = (bid % tiles_m) * BM;
+  const int G = gridDim.x;
+  int l = blockIdx.x;  // consecutive logical workgroups on one XCD
+  if ((G & 7) == 0) l = (l & 7) * (G >> 3) + (l >> 3);
 
   const int kp = (a.K + 63) & ~63;
   const v4i_t rw = buf_rsrc(a.W, (uint64_t)a.N * kp * 2);
   const v4i_t rx = buf_rsrc(a.X, (uint64_t)a.M * a.ldx * 2);
   const int lrow = lane / CPR;
   const int lchunk = chunk_pos<CPR>(lrow, lane % CPR);  // row base is a multiple of RPI
-  // weights: block (kt, n0/8 + wave * BN/32 + j) of the tiled format
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   const int vw = lane * 16;
-  const int sw_base = (n0 / 8 + wave_u * (BN / 32)) * 1024, sw_step = 1024;
   const int sw_slab = (a.N / 8) * 1024;
-  const int vx = ((m0 + wave * (BM / 4) + lrow) * (int)a.ldx + lchunk * 8) * 2;
   const int sx_step = RPI * (int)a.ldx * 2;
   const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) char*)smem;
-  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
-  const uint32_t lds_w = lds0 + wave_s * (BN / 4) * BK * 2;
-  const uint32_t lds_x = lds0 + T::W_BYTES + wave_s * (BM / 4) * BK * 2;
-
-  // load instruction q of a stage: W rows first, then X rows
-  auto issue_one = [&](int stage, int kt, int q) {
-    const uint32_t so = stage * T::STAGE;
-    if (q < T::WI) dma16(rw, vw, sw_base + kt * sw_slab + q * sw_step, lds_w + so + q * 1024);
-    else dma16(rx, vx, (q - T::WI) * sx_step + kt * BK * 2, lds_x + so + (q - T::WI) * 1024);
-  };
-  auto issue = [&](int stage, int kt) {
-#pragma unroll
-    for (int q = 0; q < T::LPS; ++q) issue_one(stage, kt, q);
-  };
-  // spread the LPS loads of a stage over the TN * BK/32 row-tile steps
-  constexpr int STEPS = TN * (BK / 32);
-  auto issue_part = [&](int stage, int kt, int step) {
-#pragma unroll
-    for (int q = step * T::LPS / STEPS; q < (step + 1) * T::LPS / STEPS; ++q)
-      issue_one(stage, kt, q);
-  };
+  const uint32_t lds_w = lds0 + wave_u * (BN / 4) * BK * 2;
+  const uint32_t lds_x = lds0 + T::W_BYTES + wave_u * (BM / 4) * BK * 2;
+  const int fr = lane & 15, g = lane >> 4;
 
   f32x4_v acc[TN][TM];
-#pragma unroll
-  for (int i = 0; i < TN; ++i)
-#pragma unroll
-    for (int j = 0; j < TM; ++j) acc[i][j] = f32x4_v{0.f, 0.f, 0.f, 0.f};
 
-  const int fr = lane & 15, g = lane >> 4;
-  const int nk = kp / BK;
+  // acc = sum over k steps [k0, k1) of tile (n0, m0)
+  auto mainloop = [&](int n0, int m0, int k0, int k1) {
 #pragma unroll
-  for (int s = 0; s < NS - 1; ++s)
-    if (s < nk) issue(s, s);
-  if (nk >= NS - 1) wait_vm<(NS - 2) * T::LPS>();
-  else wait_vm<0>();
-  wg_barrier();
-
-  for (int kt = 0; kt < nk; ++kt) {
-    const int stage = kt % NS;
-    const bool more = kt + NS - 1 < nk;
-    const bf16_t* sw = reinterpret_cast<const bf16_t*>(smem + stage * T::STAGE);
-    const bf16_t* sx = reinterpret_cast<const bf16_t*>(smem + stage * T::STAGE + T::W_BYTES);
-    // SPREAD: the next stage's loads are issued between MFMA groups (best with
-    // one wave per SIMD); otherwise all at once before the stage's MFMAs.
-    if (!SPREAD && more) issue((kt + NS - 1) % NS, kt + NS - 1);
-    ring_stage<BN, BM, BK, NS>(acc, sw, sx, wn, wm, fr, g, [&](int step) {
-      if (SPREAD && more) issue_part((kt + NS - 1) % NS, kt + NS - 1, step);
-    });
-    if (more) wait_vm<(NS - 2) * T::LPS>();
+    for (int i = 0; i < TN; ++i)
+#pragma unroll
+      for (int j = 0; j < TM; ++j) acc[i][j] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+    // weights: block (kt, n0/8 + wave * BN/32 + q) of the tiled format
+    const int sw_base = (n0 / 8 + wave_u * (BN / 32)) * 1024;
+    const int vx = ((m0 + wave * (BM / 4) + lrow) * (int)a.ldx + lchunk * 8) * 2;
+    auto issue_one = [&](int stage, int kt, int q) {
+      const uint32_t so = stage * T::STAGE;
+      if (q < T::WI) dma16(rw, vw, sw_base + kt * sw_slab + q * 1024, lds_w + so + q * 1024);
+      else dma16(rx, vx, (q - T::WI) * sx_step + kt * BK * 2, lds_x + so + (q - T::WI) * 1024);
+    };
+    // the loads of the next stage are spread over the first SPR/4 of the
+    // row-tile steps of the current stage's multiplication
+    constexpr int STEPS = TN * (BK / 32), USE = STEPS * SPR / 4;
+    static_assert(USE >= 1, "spread");
+    auto issue_part = [&](int stage, int kt, int step) {
+      if (step < USE) {
+#pragma unroll
+        for (int q = step * LPS / USE; q < (step + 1) * LPS / USE; ++q) issue_one(stage, kt, q);
+      }
+    };
+    // Step j issues the loads of step j + NS - 1 while it multiplies. The
+    // issue is behind a (uniform) branch on purpose: it splits the step into
+    // scheduling regions, without which the register allocator shuffles the
+    // accumulators between MFMAs.
+    const int n = k1 - k0;
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s)
+      if (s < n) {
+#pragma unroll
+        for (int q = 0; q < LPS; ++q) issue_one(s, k0 + s, q);
+      }
+    if (n >= NS - 1) wait_vm<(NS - 2) * LPS>();
     else wait_vm<0>();
     wg_barrier();
-  }
-
-  const int fq = g * 4;
-#pragma unroll
-  for (int j = 0; j < TM; ++j) {
-    const int m = m0 + wm * WM + j * 16 + fr;
-    if constexpr (EPI == EPI_SWIGLU) {
-#pragma unroll
-      for (int i = 0; i < TN; i += 2)
-        store_swiglu(a, m, (n0 + wn * WN + i * 16) / 2 + fq, acc[i][j], acc[i + 1][j]);
-    } else {
-#pragma unroll
-      for (int i = 0; i < TN; ++i) store4<EPI>(a, m, n0 + wn * WN + i * 16 + fq, acc[i][j]);
+    for (int j = 0; j < n; ++j) {
+      const int stage = j % NS, nst = (j + NS - 1) % NS, kn = k0 + j + NS - 1;
+      const bool more = j + NS - 1 < n;
+      const bf16_t* sw = reinterpret_cast<const bf16_t*>(smem + stage * T::STAGE);
+      const bf16_t* sx = reinterpret_cast<const bf16_t*>(smem + stage * T::STAGE + T::W_BYTES);
+      ring_stage<BN, BM, BK, NS>(acc, sw, sx, wn, wm, fr, g, [&](int step) {
+        if (more) issue_part(nst, kn, step);
+      });
+      if (more) wait_vm<(NS - 2) * LPS>();
+      else wait_vm<0>();
+      wg_barrier();
     }
+  };
+
+  auto epilogue = [&](int n0, int m0) {
+    const int fq = g * 4;
+#pragma unroll
+    for (int j = 0; j < TM; ++j) {
+      const int m = m0 + wm * WM + j * 16 + fr;
+      if constexpr (EPI == EPI_SWIGLU) {
+#pragma unroll
+        for (int i = 0; i < TN; i += 2)
+          store_swiglu(a, m, (n0 + wn * WN + i * 16) / 2 + fq, acc[i][j], acc[i + 1][j]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < TN; ++i) store4<EPI>(a, m, n0 + wn * WN + i * 16 + fq, acc[i][j]);
+      }
+    }
+  };
+
+  if constexpr (!SK) {
+    int nt, mt;
+    tile_coords(sc, l, nt, mt);
+    mainloop(nt * BN, mt * BM, 0, sc.nk);
+    epilogue(nt * BN, mt * BM);
+  } else {
+
+  // stream-K: partial tiles live at part[(2 * g + slot) * BN * BM], slot 0
+  // for a workgroup's first segment and 1 for its last, in the lane order of
+  // the accumulators (coalesced 1 KiB per fragment). They are written and
+  // read with device-scope (sc1) accesses, which are coherent across the
+  // XCDs' L2 caches on their own; a writer waits for its stores to complete
+  // before its arrival is counted, so the last arrival sees every partial
+  // without any cache-wide write-back or invalidation.
+  constexpr int TILE_F = BN * BM;
+  constexpr int kSc1 = 16;  // cache-policy bit: device scope
+  typedef unsigned u32x4_v __attribute__((ext_vector_type(4)));
+  const __amdgpu_buffer_rsrc_t rp =
+      __builtin_amdgcn_make_buffer_rsrc(a.part, 0, 0x7FFFFFFF, kRsrcWord3);
+  auto frag_off = [&](int i, int j) { return (((i * TM + j) * 4 + wave) * 64 + lane) * 16; };
+  const int64_t beg = sk_begin(l, sc.total, G), end = sk_begin(l + 1, sc.total, G);
+  for (int64_t it = beg; it < end;) {
+    const int t = (int)(it / sc.nk);
+    const int k0 = (int)(it - (int64_t)t * sc.nk);
+    const int k1 = (int)min<int64_t>(sc.nk, k0 + (end - it));
+    int nt, mt;
+    tile_coords(sc, t, nt, mt);
+    mainloop(nt * BN, mt * BM, k0, k1);
+    if (k0 > 0 || k1 < sc.nk) {
+      const int slot = it == beg ? 0 : 1;
+      const int mine = (2 * l + slot) * TILE_F * 4;
+#pragma unroll
+      for (int i = 0; i < TN; ++i)
+#pragma unroll
+        for (int j = 0; j < TM; ++j)
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_v, acc[i][j]), rp,
+                                                 frag_off(i, j), mine, kSc1);
+      const int g0 = sk_owner((int64_t)t * sc.nk, sc.total, G);
+      const int g1 = sk_owner((int64_t)(t + 1) * sc.nk - 1, sc.total, G);
+      wait_vm<0>();
+      __syncthreads();
+      if (tid == 0) {
+        const uint32_t prev =
+            __hip_atomic_fetch_add(a.flags + t, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_last = prev == (uint32_t)(g1 - g0);
+      }
+      __syncthreads();
+      if (s_last) {
+        // running sum over contributors in k order; the partials before this
+        // workgroup's own go into `pre`, the rest straight into acc (16
+        // fragments per batch of loads, 8 or 16)
+        constexpr int FR = TN * TM, HB = FR > 16 ? 8 : FR;
+#pragma unroll
+        for (int f0 = 0; f0 < FR; f0 += HB) {
+          f32x4_v pre[HB];
+          bool after = false;
+          for (int c = g0; c <= g1; ++c) {
+            if (c == l) {
+              if (c != g0) {
+#pragma unroll
+                for (int u = 0; u < HB; ++u)
+                  acc[(f0 + u) / TM][(f0 + u) % TM] = pre[u] + acc[(f0 + u) / TM][(f0 + u) % TM];
+              }
+              after = true;
+              continue;
+            }
+            const int cs = sk_begin(c, sc.total, G) / sc.nk == t ? 0 : 1;
+            f32x4_v v[HB];
+#pragma unroll
+            for (int u = 0; u < HB; ++u)
+              v[u] = __builtin_bit_cast(
+                  f32x4_v, __builtin_amdgcn_raw_buffer_load_b128(
+                               rp, frag_off((f0 + u) / TM, (f0 + u) % TM),
+                               __builtin_amdgcn_readfirstlane((2 * c + cs) * TILE_F * 4), kSc1));
+            if (after) {
+#pragma unroll
+              for (int u = 0; u < HB; ++u) acc[(f0 + u) / TM][(f0 + u) % TM] += v[u];
+            } else if (c == g0) {
+#pragma unroll
+              for (int u = 0; u < HB; ++u) pre[u] = v[u];
+            } else {
+#pragma unroll
+              for (int u = 0; u < HB; ++u) pre[u] += v[u];
+            }
+          }
+        }
+        if (tid == 0) __hip_atomic_store(a.flags + t, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        epilogue(nt * BN, mt * BM);
+      }
+    } else {
+      epilogue(nt * BN, mt * BM);
+    }
+    it += k1 - k0;
+  }
   }
 }
 
@@ -401,17 +539,53 @@ hipError_t dispatch_epi_skinny(const GemmArgs& a, int epi, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int BN, int BM, int BK, int NS, int WPE, int SPREAD>
-hipError_t dispatch_epi_ring(const GemmArgs& a, int epi, hipStream_t s) {
-  const int tiles = ((a.N + BN - 1) / BN) * ((a.M + BM - 1) / BM);
+template <int BN, int BM, int NS, int SPR, bool SK>
+hipError_t dispatch_ring(const GemmArgs& a, int epi, const GemmSched& sc, int grid, hipStream_t s) {
   switch (epi) {
-    case EPI_STORE: hipLaunchKernelGGL((gemm_ring<BN, BM, BK, NS, WPE, SPREAD, EPI_STORE>), dim3(tiles), dim3(256), 0, s, a); break;
-    case EPI_RESID: hipLaunchKernelGGL((gemm_ring<BN, BM, BK, NS, WPE, SPREAD, EPI_RESID>), dim3(tiles), dim3(256), 0, s, a); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_ring<BN, BM, BK, NS, WPE, SPREAD, EPI_SWIGLU>), dim3(tiles), dim3(256), 0, s, a); break;
-    case EPI_F32: hipLaunchKernelGGL((gemm_ring<BN, BM, BK, NS, WPE, SPREAD, EPI_F32>), dim3(tiles), dim3(256), 0, s, a); break;
+    case EPI_STORE: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_STORE>), dim3(grid), dim3(256), 0, s, a, sc); break;
+    case EPI_RESID: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_RESID>), dim3(grid), dim3(256), 0, s, a, sc); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_SWIGLU>), dim3(grid), dim3(256), 0, s, a, sc); break;
+    case EPI_F32: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_F32>), dim3(grid), dim3(256), 0, s, a, sc); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+struct RingCfg {
+  const char* name;
+  int bn, bm;
+  bool sk_ok;  // has a stream-K build
+};
+const RingCfg kRing[] = {{"256x256", 256, 256, false}, {"256x256e", 256, 256, false},
+                         {"256x128", 256, 128, true}, {"128x128", 128, 128, true}};
+
+// 256 x 256: 2 stages (128 KiB of LDS); "e" issues the next stage's loads
+// in the first 3/4 of the current one. 256 x 128: 3 stages. 128 x 128: 4.
+hipError_t launch_ring(const RingCfg& c, const GemmArgs& a, int epi, const GemmSched& sc,
+                       int grid, hipStream_t s) {
+  if (c.bn == 256 && c.bm == 256) {
+    if (c.name[7] == 'e') return dispatch_ring<256, 256, 2, 3, false>(a, epi, sc, grid, s);
+    return dispatch_ring<256, 256, 2, 4, false>(a, epi, sc, grid, s);
+  }
+  if (c.bn == 256 && c.bm == 128)
+    return sc.sk ? dispatch_ring<256, 128, 3, 4, true>(a, epi, sc, grid, s)
+                 : dispatch_ring<256, 128, 3, 4, false>(a, epi, sc, grid, s);
+  return sc.sk ? dispatch_ring<128, 128, 4, 4, true>(a, epi, sc, grid, s)
+               : dispatch_ring<128, 128, 4, 4, false>(a, epi, sc, grid, s);
+}
+
+int device_cus() {
+  static int cus[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (!cus[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n <= 0)
+      n = 256;
+    cus[dev] = n;
+  }
+  return cus[dev];
 }
 
 const char* kEpiName[4] = {"store", "resid", "swiglu", "f32"};
@@ -457,21 +631,72 @@ hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info) {
     }
     snprintf(name, sizeof name, "gemm_skinny_%s", kEpiName[epi]);
   } else {
-    // Tile choice; HS_GEMM_CFG forces one (tuning only).
+    // Configuration by a small cost model: a data-parallel launch takes
+    // rounds x (tile flops / per-CU rate of its tile shape); a stream-K launch
+    // takes (flops / CUs) / its rate plus a fixed cost for the pipeline
+    // start-ups and the partial-tile reductions. The rates are per-CU
+    // TFLOP/s measured on MI355X with weights streamed from HBM.
+    // HS_GEMM_CFG="<tile>[,dp|,sk][,g<n>]" forces a choice (tuning only).
+    const int cus = device_cus();
+    const int nk = (int)(kp / 64);
+    struct Cand { const RingCfg* c; bool sk; double us; };
+    auto tiles_of = [&](const RingCfg& c) {
+      return (long)((a.N + c.bn - 1) / c.bn) * ((a.M + c.bm - 1) / c.bm);
+    };
+    auto sk_room = [&](const RingCfg& c, long tiles) {
+      const long g = std::min<long>(cus, tiles * nk / 4);
+      return c.sk_ok && g >= 1 && a.part && a.flags && tiles <= a.flags_n &&
+             2 * g * (int64_t)c.bn * c.bm <= a.part_floats;
+    };
+    const Cand cands[] = {
+        {&kRing[1], false, 0}, {&kRing[2], false, 0}, {&kRing[3], false, 0}, {&kRing[3], true, 0}};
+    const double rate_dp[] = {4.6, 4.05, 3.05}, rate_sk = 3.0, sk_fixed_us = 10.0;
+    const RingCfg* cfg = nullptr;
+    bool sk = false;
+    double best = 1e300;
+    for (int i = 0; i < 4; ++i) {
+      const RingCfg& c = *cands[i].c;
+      const long tiles = tiles_of(c);
+      double us;
+      if (!cands[i].sk) {
+        const long rounds = (tiles + cus - 1) / cus;
+        us = rounds * (2.0 * kp * c.bn * c.bm) / (rate_dp[i] * 1e6);
+      } else {
+        if (!sk_room(c, tiles)) continue;
+        us = (2.0 * a.M * (double)a.N * kp / cus) / (rate_sk * 1e6) + sk_fixed_us;
+      }
+      if (us < best) {
+        best = us;
+        cfg = &c;
+        sk = cands[i].sk;
+      }
+    }
+    int group = 8;
     static const char* force = getenv("HS_GEMM_CFG");
-    const long b256 = (long)((a.N + 255) / 256) * ((a.M + 255) / 256);
-    const long t256x128 = (long)((a.N + 255) / 256) * ((a.M + 127) / 128);
-    std::string cfg;
-    if (force && *force) cfg = force;
-    else if (b256 >= 256) cfg = "r256x256";       // large M: 1 wave / SIMD, 2 stages
-    else if (t256x128 >= 160) cfg = "r256x128s3"; // mid-size: 3-stage ring
-    else cfg = "r128x64s4";                       // few tiles: smaller ones, 4 stages
-    if (cfg == "r256x256") e = dispatch_epi_ring<256, 256, 64, 2, 1, 1>(a, epi, s);
-    else if (cfg == "r256x128s3") e = dispatch_epi_ring<256, 128, 64, 3, 1, 1>(a, epi, s);
-    else if (cfg == "r128x128") e = dispatch_epi_ring<128, 128, 64, 2, 2, 0>(a, epi, s);
-    else if (cfg == "r128x64") e = dispatch_epi_ring<128, 64, 64, 3, 2, 0>(a, epi, s);
-    else e = dispatch_epi_ring<128, 64, 64, 4, 1, 1>(a, epi, s);
-    snprintf(name, sizeof name, "gemm_%s_%s", cfg.c_str(), kEpiName[epi]);
+    if (force && *force) {
+      std::string f(force);
+      for (const RingCfg& c : kRing)  // longest matching name wins
+        if (f.compare(0, strlen(c.name), c.name) == 0 &&
+            (f.size() == strlen(c.name) || f[strlen(c.name)] == ','))
+          cfg = &c;
+      if (f.find(",dp") != std::string::npos) sk = false;
+      if (f.find(",sk") != std::string::npos) sk = true;
+      const size_t gp = f.find(",g");
+      if (gp != std::string::npos) group = std::max(1, atoi(f.c_str() + gp + 2));
+    }
+    GemmSched sc;
+    sc.tiles_n = (a.N + cfg->bn - 1) / cfg->bn;
+    sc.tiles_m = (a.M + cfg->bm - 1) / cfg->bm;
+    sc.nk = nk;
+    sc.group_n = group;
+    const long tiles = (long)sc.tiles_n * sc.tiles_m;
+    sc.total = (int64_t)tiles * nk;
+    if (sk && !sk_room(*cfg, tiles)) sk = false;
+    sc.sk = sk ? 1 : 0;
+    const long grid = sk ? std::min<long>(cus, sc.total / 4) : tiles;
+    if (grid > 0x7FFFFFFF) return hipErrorInvalidValue;
+    e = launch_ring(*cfg, a, epi, sc, (int)grid, s);
+    snprintf(name, sizeof name, "gemm_r%s%s_%s", cfg->name, sk ? "sk" : "", kEpiName[epi]);
   }
   if (info) {
     info->name = name;

@@ -13,6 +13,39 @@
 using namespace hs;
 
 namespace {
+// Split-k workspace of hs_k_gemm, one per device, allocated on first use and
+// kept until the process ends (calls on one device must not overlap).
+struct GemmWs {
+  float* part = nullptr;
+  uint32_t* flags = nullptr;
+};
+constexpr int64_t kWsPartFloats = 2ll * 256 * 256 * 256;  // 2 slots x 256 workgroups x 256x256
+constexpr int64_t kWsFlags = 1 << 16;
+
+hs_status gemm_ws(GemmWs** out) {
+  static GemmWs ws[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+    return fail(HS_EHIP, "hipGetDevice failed");
+  GemmWs& w = ws[dev];
+  if (!w.part) {
+    float* p = nullptr;
+    uint32_t* f = nullptr;
+    if (hipMalloc(&p, kWsPartFloats * sizeof(float)) != hipSuccess) return fail(HS_ENOMEM, "gemm workspace");
+    if (hipMalloc(&f, kWsFlags * sizeof(uint32_t)) != hipSuccess ||
+        hipMemset(f, 0, kWsFlags * sizeof(uint32_t)) != hipSuccess ||
+        hipDeviceSynchronize() != hipSuccess) {
+      (void)hipFree(p);
+      if (f) (void)hipFree(f);
+      return fail(HS_ENOMEM, "gemm workspace");
+    }
+    w.part = p;
+    w.flags = f;
+  }
+  *out = &w;
+  return HS_OK;
+}
+
 hs_status launched(hipError_t e, const char* what) {
   if (e == hipErrorInvalidValue) return fail(HS_EINVAL, std::string(what) + ": unsupported shape");
   if (e != hipSuccess) return fail(HS_EHIP, std::string(what) + ": " + hipGetErrorString(e));
@@ -27,6 +60,13 @@ extern "C" hs_status hs_k_gemm(const void* X, int64_t ldx, const void* Wt, void*
     if (!X || !Wt || !Y) return fail(HS_EINVAL, "null operand");
     GemmArgs a{static_cast<const bf16_t*>(X), ldx, static_cast<const bf16_t*>(Wt), Y, ldy,
                static_cast<const bf16_t*>(R), ldr, M, N, K};
+    GemmWs* ws = nullptr;
+    const hs_status r = gemm_ws(&ws);
+    if (r != HS_OK) return r;
+    a.part = ws->part;
+    a.part_floats = kWsPartFloats;
+    a.flags = ws->flags;
+    a.flags_n = kWsFlags;
     return launched(gemm(a, epi, static_cast<hipStream_t>(stream), nullptr), "gemm");
   } catch (...) {
     return fail(HS_EINVAL, "unexpected internal error");

@@ -102,6 +102,9 @@ struct hs_stage {
   bf16_t *w_x = nullptr, *w_u = nullptr, *w_qkv = nullptr, *w_attn = nullptr, *w_act = nullptr,
          *w_last = nullptr;
   float *w_logits = nullptr, *w_part_o = nullptr, *w_part_ml = nullptr;
+  float* w_gpart = nullptr;       // split-k partial tiles of the projection GEMMs
+  uint32_t* w_gflags = nullptr;   // their per-tile arrival counters (kept at zero)
+  int64_t gpart_floats = 0, gflags_n = 0;
   float *d_cos = nullptr, *d_sin = nullptr;
   int32_t max_splits = 0;
   int64_t ws_rows = 0;
@@ -185,6 +188,17 @@ hipEvent_t pool_event(hs_stage* st) {
   hipEvent_t e = nullptr;
   if (hipEventCreate(&e) != hipSuccess) return nullptr;
   return e;
+}
+
+// Projection GEMM arguments with the stage's split-k workspace attached.
+GemmArgs gemm_args(const hs_stage* st, const bf16_t* X, int64_t ldx, const bf16_t* W, void* Y,
+                   int64_t ldy, const bf16_t* R, int64_t ldr, int M, int N, int K) {
+  GemmArgs g{X, ldx, W, Y, ldy, R, ldr, M, N, K};
+  g.part = st->w_gpart;
+  g.part_floats = st->gpart_floats;
+  g.flags = st->w_gflags;
+  g.flags_n = st->gflags_n;
+  return g;
 }
 
 // Launch through a kernel launcher, bracketed by events when timing is on.
@@ -363,7 +377,7 @@ hs_status layer_forward(hs_stage* st, int l, bf16_t* x, const LayerCall& c, hipS
   });
   if (r != HS_OK) return r;
   r = run(st, s, [&](LaunchInfo* i) {
-    GemmArgs g{st->w_u, H, W(st, ls.qkv), st->w_qkv, NQKV, nullptr, 0, c.T, NQKV, H};
+    GemmArgs g = gemm_args(st, st->w_u, H, W(st, ls.qkv), st->w_qkv, NQKV, nullptr, 0, c.T, NQKV, H);
     return gemm(g, EPI_STORE, s, i);
   });
   if (r != HS_OK) return r;
@@ -392,7 +406,7 @@ hs_status layer_forward(hs_stage* st, int l, bf16_t* x, const LayerCall& c, hipS
   }
   if (r != HS_OK) return r;
   r = run(st, s, [&](LaunchInfo* i) {
-    GemmArgs g{st->w_attn, QD, W(st, ls.o), x, H, x, H, c.T, H, QD};
+    GemmArgs g = gemm_args(st, st->w_attn, QD, W(st, ls.o), x, H, x, H, c.T, H, QD);
     return gemm(g, EPI_RESID, s, i);
   });
   if (r != HS_OK) return r;
@@ -401,12 +415,12 @@ hs_status layer_forward(hs_stage* st, int l, bf16_t* x, const LayerCall& c, hipS
   });
   if (r != HS_OK) return r;
   r = run(st, s, [&](LaunchInfo* i) {
-    GemmArgs g{st->w_u, H, W(st, ls.gateup), st->w_act, FA, nullptr, 0, c.T, 2 * F, H};
+    GemmArgs g = gemm_args(st, st->w_u, H, W(st, ls.gateup), st->w_act, FA, nullptr, 0, c.T, 2 * F, H);
     return gemm(g, EPI_SWIGLU, s, i);
   });
   if (r != HS_OK) return r;
   return run(st, s, [&](LaunchInfo* i) {
-    GemmArgs g{st->w_act, FA, W(st, ls.down), x, H, x, H, c.T, H, F};
+    GemmArgs g = gemm_args(st, st->w_act, FA, W(st, ls.down), x, H, x, H, c.T, H, F);
     return gemm(g, EPI_RESID, s, i);
   });
 }
@@ -422,7 +436,7 @@ hs_status head_forward(hs_stage* st, const bf16_t* x, const int32_t* rows, int n
   if (r != HS_OK) return r;
   float* lg = logits ? logits : st->w_logits;
   r = run(st, s, [&](LaunchInfo* i) {
-    GemmArgs g{st->w_last, H, W(st, st->L.lm_head), lg, m.vocab, nullptr, 0, n, m.vocab, H};
+    GemmArgs g = gemm_args(st, st->w_last, H, W(st, st->L.lm_head), lg, m.vocab, nullptr, 0, n, m.vocab, H);
     return gemm(g, EPI_F32, s, i);
   });
   if (r != HS_OK) return r;
@@ -585,9 +599,19 @@ extern "C" hs_status hs_stage_create(const hs_model_cfg* cfg, int32_t layer_begi
   const uint64_t R = (uint64_t)st->ws_rows, S = (uint64_t)opts->max_seqs;
   uint64_t off = 0;
   std::vector<uint64_t> offs;
+  // split-k workspace: two 256 x 128 fp32 partial tiles per CU, a counter
+  // per 128 x 64 output tile of the widest projection
+  int cus = 256;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess ||
+      cus <= 0)
+    cus = 256;
+  const int64_t max_n = std::max<int64_t>(std::max(NQKV, 2 * F), std::max(H, V));
+  st->gpart_floats = R > 64 ? 2ll * cus * 256 * 128 : 0;
+  st->gflags_n = R > 64 ? ((max_n + 127) / 128) * (int64_t)((R + 63) / 64) : 0;
   for (uint64_t sz : {R * H * 2, R * H * 2, R * NQKV * 2, R * QD * 2, R * round64(F) * 2, S * H * 2,
                       S * V * 4, S * m.n_heads * st->max_splits * (uint64_t)D * 4,
-                      S * m.n_heads * st->max_splits * 2 * 4}) {
+                      S * m.n_heads * st->max_splits * 2 * 4, (uint64_t)st->gpart_floats * 4,
+                      (uint64_t)st->gflags_n * 4}) {
     offs.push_back(off);
     off = al(off + sz);
   }
@@ -605,6 +629,8 @@ extern "C" hs_status hs_stage_create(const hs_model_cfg* cfg, int32_t layer_begi
   st->w_logits = reinterpret_cast<float*>(st->d_ws + offs[6]);
   st->w_part_o = reinterpret_cast<float*>(st->d_ws + offs[7]);
   st->w_part_ml = reinterpret_cast<float*>(st->d_ws + offs[8]);
+  st->w_gpart = st->gpart_floats ? reinterpret_cast<float*>(st->d_ws + offs[9]) : nullptr;
+  st->w_gflags = st->gflags_n ? reinterpret_cast<uint32_t*>(st->d_ws + offs[10]) : nullptr;
 
   // RoPE table: angle pos * base^(-2i/D) in double, stored as float.
   {

@@ -63,6 +63,43 @@ def test_gemm(M, N, K, epi):
     assert err <= tol, (err, scale)
 
 
+# 7B-shape projections at a 512-token prompt: few output tiles, so their k
+# ranges are split across workgroups (stream-K). Rows are sampled for the
+# float64 reference; two calls must agree bitwise.
+@pytest.mark.parametrize("N,K,epi", [(12288, 4096, "store"), (4096, 4096, "resid"),
+                                     (22016, 4096, "swiglu"), (4096, 11008, "resid")])
+def test_gemm_split_k_shapes(N, K, epi):
+    torch = G.torch()
+    hs = _hs()
+    M = 512
+    rng = np.random.default_rng(N + K)
+    X = gen.round_to_bf16(rng.standard_normal((M, K)).astype(np.float32))
+    Wt = gen.round_to_bf16((rng.standard_normal((N, K)) * 0.02).astype(np.float32))
+    dX = G.to_dev_bf16(X)
+    dW = torch.from_numpy(G.tile_bits(gen.to_bf16_bits(Wt)).view(np.int16)).cuda()
+    ncol = N // 2 if epi == "swiglu" else N
+    R = gen.round_to_bf16(rng.standard_normal((M, ncol)).astype(np.float32))
+    outs = []
+    for _ in range(2):
+        Y = G.to_dev_bf16(R) if epi == "resid" else torch.zeros((M, ncol), dtype=torch.bfloat16, device="cuda")
+        hs.hs_k_gemm(dX.data_ptr(), K, dW.data_ptr(), Y.data_ptr(), ncol,
+                     Y.data_ptr() if epi == "resid" else 0, ncol, M, N, K, epi, G.stream_ptr())
+        torch.cuda.synchronize()
+        outs.append(G.from_dev_bf16(Y))
+    assert np.array_equal(outs[0], outs[1])
+    rows = np.sort(rng.choice(M, 24, replace=False))
+    acc = X[rows].astype(np.float64) @ Wt.astype(np.float64).T
+    if epi == "swiglu":
+        idx = np.arange(ncol)
+        ref = silu(acc[:, (idx // 16) * 32 + idx % 16]) * acc[:, (idx // 16) * 32 + 16 + idx % 16]
+    elif epi == "resid":
+        ref = R[rows] + acc
+    else:
+        ref = acc
+    err = np.abs(outs[0][rows] - ref).max()
+    assert err <= 8e-3 * np.abs(ref).max(), err
+
+
 @pytest.mark.parametrize("lens,nh,nkv,d", [
     ([1], 4, 4, 64), ([5, 64, 65], 4, 2, 64), ([130, 7, 300], 4, 4, 128),
     ([257], 8, 2, 128), ([64, 128, 1, 33], 2, 1, 128),
