@@ -73,7 +73,7 @@ def traffic_from_profiles(kernel):
     return k.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(wl, x_f32, stage_range):
+def cpu_baseline(wl, x_f32, stage_range, min_seconds=12.0):
     """The oracle, as it stands, on the same prefill (all 512 tokens, all 8
     layers of the stage), on this host's cores."""
     import numpy as np
@@ -86,15 +86,19 @@ def cpu_baseline(wl, x_f32, stage_range):
         for k in ("wq", "wk", "wv", "wo", "wgate", "wup", "wdown"):
             W(l, k)
     st = Stage(cfg, W, b, e)
-    t0 = time.perf_counter()
-    st.prefill([0], [x_f32.shape[0]], x_f32)
-    dt = time.perf_counter() - t0
+    reps, dt = 0, 0.0
+    while dt < min_seconds:            # repeat the prefill for a bounded sample
+        t0 = time.perf_counter()
+        st.prefill([reps], [x_f32.shape[0]], x_f32)
+        dt += time.perf_counter() - t0
+        st.drop(reps)
+        reps += 1
     threads = max([p.get("num_threads", 1) for p in threadpool_info()
                    if p.get("user_api") == "blas"] or [1])
-    return {"value": round(x_f32.shape[0] / dt, 2), "unit": "tok/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": f"full prefill of the {x_f32.shape[0]}-token prompt through layers "
-                      f"{b}-{e - 1} (numpy float32, {dt:.2f} s)",
+    return {"value": round(reps * x_f32.shape[0] / dt, 2), "unit": "tok/s",
+            "cores": int(threads), "kind": "oracle",
+            "sample": f"{reps} full prefills of the {x_f32.shape[0]}-token prompt through "
+                      f"layers {b}-{e - 1} (numpy float32, {dt:.1f} s in total)",
             "host_cpus": os.cpu_count()}
 
 
@@ -183,66 +187,74 @@ def main():
     log(f"[bench] cold TTFT {t_cold * 1e3:.2f} ms, load only {t_load * 1e3:.2f} ms")
 
     # -------------------------------------------------------- warm prefill
-    for _ in range(args.warmup):
-        i = prefill_once()
+    # Warm-up steps run with every launch timed: they give the per-kernel
+    # breakdown and name the dominant kernel. The timed steps then bracket
+    # only that kernel's launch site with events (events between
+    # back-to-back kernels cost time of their own).
+    def run_steps(k):
+        ids = []
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        t0 = time.perf_counter()
+        for _ in range(k):
+            ids.append(prefill_once())
+            if len(ids) >= 3:                # keep KV blocks bounded
+                hs.hs_seq_free(st.h, ids.pop(0))
+        ev1.record(stream)
         stream.synchronize()
-        hs.hs_seq_free(st.h, i)
+        wall = time.perf_counter() - t0
+        for i in ids:
+            hs.hs_seq_free(st.h, i)
+        return max(ev0.elapsed_time(ev1), wall * 1e3) / k
+
     hs.hs_stage_read_timing(st.h)            # reset counters
+    hs.hs_stage_set_timing_sites(st.h, None)
     hs.hs_stage_set_timing(st.h, 1)
-    ids = []
-    torch.cuda.synchronize()
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
-    ev0.record(stream)
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        ids.append(prefill_once())
-        if len(ids) >= 3:                    # keep KV blocks bounded
-            hs.hs_seq_free(st.h, ids.pop(0))
-    ev1.record(stream)
-    stream.synchronize()
-    wall = time.perf_counter() - t0
-    torch.cuda.synchronize()
+    run_steps(max(args.warmup, 1))
     hs.hs_stage_set_timing(st.h, 0)
     stats = hs.hs_stage_read_timing(st.h)
-    for i in ids:
-        hs.hs_seq_free(st.h, i)
-    gpu_ms = ev0.elapsed_time(ev1)
-    ms_step = max(gpu_ms, wall * 1e3) / args.steps
-    tok_s = P / (ms_step / 1e3)
-    t_prefill = ms_step / 1e3
+    nw = max(args.warmup, 1)
     kern_ms = sum(s["total_ms"] for s in stats)
-    flops_step = sum(s["flops"] for s in stats) / args.steps
-    log(f"[bench] warm prefill {ms_step:.3f} ms/step = {tok_s:,.0f} tok/s "
-        f"({flops_step / (ms_step / 1e3) / 1e12:.0f} TFLOP/s over the step)")
+    flops_step = sum(s["flops"] for s in stats) / nw
+    log("[bench] warm-up steps with every launch timed:")
     for s in sorted(stats, key=lambda s: -s["total_ms"]):
         avg = s["total_ms"] / s["launches"]
         rate = (s["flops"] / s["launches"]) / (avg / 1e3) / 1e12 if s["flops"] else 0
         bw = (s["bytes"] / s["launches"]) / (avg / 1e3) / 1e9 if s["bytes"] else 0
-        log(f"[bench]   {s['name']:<28} x{s['launches'] // args.steps:<3} avg {avg * 1e3:8.1f} us "
-            f"{100 * s['total_ms'] / kern_ms:5.1f}%  {rate:7.1f} TFLOP/s {bw:7.0f} GB/s")
-    # the same steps without per-kernel events (their cost inside the step)
-    ids = []
-    ev0.record(stream)
-    for _ in range(args.steps):
-        ids.append(prefill_once())
-        if len(ids) >= 3:
-            hs.hs_seq_free(st.h, ids.pop(0))
-    ev1.record(stream)
-    stream.synchronize()
-    for i in ids:
-        hs.hs_seq_free(st.h, i)
-    ms_step_plain = ev0.elapsed_time(ev1) / args.steps
-    log(f"[bench] same steps without kernel events: {ms_step_plain:.3f} ms/step")
+        log(f"[bench]   {s['name']:<28} {s['site']:<10} x{s['launches'] // nw:<3} avg "
+            f"{avg * 1e3:8.1f} us {100 * s['total_ms'] / kern_ms:5.1f}%  {rate:7.1f} TFLOP/s "
+            f"{bw:7.0f} GB/s")
     dom = max(stats, key=lambda s: s["total_ms"])
+
+    hs.hs_stage_set_timing_sites(st.h, dom["site"])
+    hs.hs_stage_set_timing(st.h, 1)
+    ms_step = run_steps(args.steps)
+    hs.hs_stage_set_timing(st.h, 0)
+    hs.hs_stage_set_timing_sites(st.h, None)
+    timed = [s for s in hs.hs_stage_read_timing(st.h)
+             if s["name"] == dom["name"] and s["site"] == dom["site"]]
+    assert timed and timed[0]["launches"] == args.steps * dom["launches"] // nw
+    dom = timed[0]
+    tok_s = P / (ms_step / 1e3)
+    t_prefill = ms_step / 1e3
+    log(f"[bench] warm prefill {ms_step:.3f} ms/step = {tok_s:,.0f} tok/s "
+        f"({flops_step / (ms_step / 1e3) / 1e12:.0f} TFLOP/s over the step)")
+    ms_step_plain = run_steps(args.steps)
+    log(f"[bench] same steps without any kernel events: {ms_step_plain:.3f} ms/step")
     dom_avg_s = dom["total_ms"] / dom["launches"] / 1e3
     dom_flops = dom["flops"] / dom["launches"]
     achieved = dom_flops / dom_avg_s / 1e12
+    log(f"[bench] dominant kernel {dom['name']} ({dom['site']}): {dom_avg_s * 1e6:.1f} us, "
+        f"{achieved:.0f} TFLOP/s in the timed steps")
     roofline = {"bound": "mfma", "kernel": dom["name"],
                 "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                 "traffic": traffic_from_profiles(dom["name"]),
                 "flops_per_launch": dom_flops, "avg_launch_us": round(dom_avg_s * 1e6, 2)}
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
 
     # ------------------------------------------------------------- decode
     i = prefill_once()
@@ -307,6 +319,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": base,
         "ms_per_step_without_kernel_events": round(ms_step_plain, 4),
+        "timed_site": dom["site"],
         "prefill_mfma_frac_step": round(flops_step / t_prefill / 1e12 / PEAK_BF16_TFLOPS, 4),
         "cold_ttft_ms": round(t_cold * 1e3, 3),
         "cold_load_only_ms": round(t_load * 1e3, 3),

@@ -329,14 +329,21 @@ hs_status hs_kv_blob_describe(const void* host_blob, uint64_t avail,
                               hs_kv_blob_info* out);
 
 /* ------------------------------------------------------------------------
- * Measurement. When timing is on, every kernel launch of the stage is
- * bracketed by HIP events on its stream. hs_stage_read_timing waits for the
- * stage, then reports per kernel: launches, total milliseconds and the
- * algorithmic flops and HBM bytes of those launches; and resets the
- * counters.
+ * Measurement. When timing is on, the stage's kernel launches are bracketed
+ * by HIP events on their stream: every launch, or only those of the launch
+ * sites named by hs_stage_set_timing_sites (a comma-separated list of
+ * "embed", "attn_norm", "qkv", "rope_kv", "attn", "o_proj", "ffn_norm",
+ * "gate_up", "down", "final_norm", "lm_head", "argmax", "kv_copy"; NULL or
+ * "" = every site). Events between back-to-back kernels cost time of their
+ * own, so timing a few sites disturbs a step less than timing all of them.
+ * hs_stage_read_timing waits for the stage, then reports per (kernel, launch
+ * site) pair: launches, total milliseconds and the algorithmic flops and
+ * HBM bytes of those launches; and resets the counters. `n` receives the
+ * number of pairs, of which min(n, cap) are written.
  */
 typedef struct {
   char name[48];
+  char site[16];
   int64_t launches;
   double total_ms;
   double flops;
@@ -344,6 +351,7 @@ typedef struct {
 } hs_kernel_stat;
 
 hs_status hs_stage_set_timing(hs_stage* st, int32_t enable);
+hs_status hs_stage_set_timing_sites(hs_stage* st, const char* sites);
 hs_status hs_stage_read_timing(hs_stage* st, hs_kernel_stat* out, int32_t cap,
                                int32_t* n);
 

@@ -54,12 +54,13 @@ struct Chunk {
 };
 
 struct Pending {
-  std::string name;
+  std::string name, site;
   hipEvent_t a, b;
   double flops, bytes;
 };
 
 struct Stat {
+  std::string name, site;
   int64_t launches = 0;
   double ms = 0, flops = 0, bytes = 0;
 };
@@ -125,6 +126,7 @@ struct hs_stage {
   bool desc_used = false;
 
   bool timing = false;
+  std::string timing_sites;  // ",site,site," or empty for every site
   std::vector<Pending> pending;
   std::map<std::string, Stat> stats;
   std::vector<hipEvent_t> ev_pool;
@@ -201,11 +203,20 @@ GemmArgs gemm_args(const hs_stage* st, const bf16_t* X, int64_t ldx, const bf16_
   return g;
 }
 
-// Launch through a kernel launcher, bracketed by events when timing is on.
+// Launch through a kernel launcher, bracketed by events when timing is on
+// for this call site.
+bool timed_site(const hs_stage* st, const char* site) {
+  if (!st->timing) return false;
+  if (st->timing_sites.empty()) return true;
+  const std::string key = std::string(",") + site + ",";
+  return st->timing_sites.find(key) != std::string::npos;
+}
+
 template <typename F>
-hs_status run(hs_stage* st, hipStream_t s, F&& launch) {
+hs_status run(hs_stage* st, hipStream_t s, const char* site, F&& launch) {
   hipEvent_t a = nullptr, b = nullptr;
-  if (st->timing) {
+  const bool timed = timed_site(st, site);
+  if (timed) {
     a = pool_event(st);
     b = pool_event(st);
     if (!a || !b) return fail(HS_EHIP, "event creation failed");
@@ -214,9 +225,9 @@ hs_status run(hs_stage* st, hipStream_t s, F&& launch) {
   LaunchInfo info{"", 0, 0};
   hipError_t e = launch(&info);
   if (e != hipSuccess) return fail(HS_EHIP, hip_msg(info.name && *info.name ? info.name : "kernel launch", e));
-  if (st->timing) {
+  if (timed) {
     HIPTRY(hipEventRecord(b, s));
-    st->pending.push_back(Pending{info.name ? info.name : "?", a, b, info.flops, info.bytes});
+    st->pending.push_back(Pending{info.name ? info.name : "?", site, a, b, info.flops, info.bytes});
   }
   return HS_OK;
 }
@@ -372,30 +383,30 @@ hs_status layer_forward(hs_stage* st, int l, bf16_t* x, const LayerCall& c, hipS
   const int FA = (int)round64(F);  // activation row stride: zero columns up to a multiple of 64
   const int NQKV = (m.n_heads + 2 * m.n_kv_heads) * D, QD = m.n_heads * D;
   hs_status r;
-  r = run(st, s, [&](LaunchInfo* i) {
+  r = run(st, s, "attn_norm", [&](LaunchInfo* i) {
     return rmsnorm(x, H, nullptr, c.T, H, W(st, ls.attn_norm), m.rms_eps, st->w_u, H, s, i);
   });
   if (r != HS_OK) return r;
-  r = run(st, s, [&](LaunchInfo* i) {
+  r = run(st, s, "qkv", [&](LaunchInfo* i) {
     GemmArgs g = gemm_args(st, st->w_u, H, W(st, ls.qkv), st->w_qkv, NQKV, nullptr, 0, c.T, NQKV, H);
     return gemm(g, EPI_STORE, s, i);
   });
   if (r != HS_OK) return r;
-  r = run(st, s, [&](LaunchInfo* i) {
+  r = run(st, s, "rope_kv", [&](LaunchInfo* i) {
     RopeKvArgs a{st->w_qkv, NQKV, c.pos, c.slot, st->d_cos, st->d_sin, pool(st, l),
                  c.T, m.n_heads, m.n_kv_heads, D, st->opts.max_ctx};
     return rope_kv(a, s, i);
   });
   if (r != HS_OK) return r;
   if (!c.decode) {
-    r = run(st, s, [&](LaunchInfo* i) {
+    r = run(st, s, "attn", [&](LaunchInfo* i) {
       AttnPrefillArgs a{st->w_qkv, NQKV, st->w_attn, QD, c.cu, c.tiles, c.n_tiles,
                         m.n_heads, m.n_kv_heads, D, c.attn_waves, 16 * c.attn_waves,
                         c.attn_flops};
       return attn_prefill(a, s, i);
     });
   } else {
-    r = run(st, s, [&](LaunchInfo* i) {
+    r = run(st, s, "attn", [&](LaunchInfo* i) {
       AttnDecodeArgs a{st->w_qkv, NQKV, pool(st, l), c.bt, c.ctx, st->w_part_o, st->w_part_ml,
                        st->w_attn, QD, c.T, m.n_heads, m.n_kv_heads, D, st->max_blocks_per_seq,
                        st->max_splits, c.call_splits, c.kv_read_bytes};
@@ -405,21 +416,21 @@ hs_status layer_forward(hs_stage* st, int l, bf16_t* x, const LayerCall& c, hipS
     });
   }
   if (r != HS_OK) return r;
-  r = run(st, s, [&](LaunchInfo* i) {
+  r = run(st, s, "o_proj", [&](LaunchInfo* i) {
     GemmArgs g = gemm_args(st, st->w_attn, QD, W(st, ls.o), x, H, x, H, c.T, H, QD);
     return gemm(g, EPI_RESID, s, i);
   });
   if (r != HS_OK) return r;
-  r = run(st, s, [&](LaunchInfo* i) {
+  r = run(st, s, "ffn_norm", [&](LaunchInfo* i) {
     return rmsnorm(x, H, nullptr, c.T, H, W(st, ls.ffn_norm), m.rms_eps, st->w_u, H, s, i);
   });
   if (r != HS_OK) return r;
-  r = run(st, s, [&](LaunchInfo* i) {
+  r = run(st, s, "gate_up", [&](LaunchInfo* i) {
     GemmArgs g = gemm_args(st, st->w_u, H, W(st, ls.gateup), st->w_act, FA, nullptr, 0, c.T, 2 * F, H);
     return gemm(g, EPI_SWIGLU, s, i);
   });
   if (r != HS_OK) return r;
-  return run(st, s, [&](LaunchInfo* i) {
+  return run(st, s, "down", [&](LaunchInfo* i) {
     GemmArgs g = gemm_args(st, st->w_act, FA, W(st, ls.down), x, H, x, H, c.T, H, F);
     return gemm(g, EPI_RESID, s, i);
   });
@@ -430,17 +441,17 @@ hs_status head_forward(hs_stage* st, const bf16_t* x, const int32_t* rows, int n
                        int32_t* out, hipStream_t s) {
   const hs_model_cfg& m = st->cfg;
   const int H = m.hidden;
-  hs_status r = run(st, s, [&](LaunchInfo* i) {
+  hs_status r = run(st, s, "final_norm", [&](LaunchInfo* i) {
     return rmsnorm(x, H, rows, n, H, W(st, st->L.final_norm), m.rms_eps, st->w_last, H, s, i);
   });
   if (r != HS_OK) return r;
   float* lg = logits ? logits : st->w_logits;
-  r = run(st, s, [&](LaunchInfo* i) {
+  r = run(st, s, "lm_head", [&](LaunchInfo* i) {
     GemmArgs g = gemm_args(st, st->w_last, H, W(st, st->L.lm_head), lg, m.vocab, nullptr, 0, n, m.vocab, H);
     return gemm(g, EPI_F32, s, i);
   });
   if (r != HS_OK) return r;
-  return run(st, s, [&](LaunchInfo* i) { return argmax_rows(lg, n, m.vocab, out, s, i); });
+  return run(st, s, "argmax", [&](LaunchInfo* i) { return argmax_rows(lg, n, m.vocab, out, s, i); });
 }
 
 bool is_device_ptr(const void* p) {
@@ -499,7 +510,7 @@ hs_status copy_units(hs_stage* st, const Units& u, int zero_tail, hipStream_t s,
   const uint64_t* ddst = reinterpret_cast<const uint64_t*>(st->d_desc + o_dst);
   const int32_t* dval = reinterpret_cast<const int32_t*>(st->d_desc + o_val);
   if (n > 0) {
-    r = run(st, s, [&](LaunchInfo* i) {
+    r = run(st, s, "kv_copy", [&](LaunchInfo* i) {
       return kv_copy(dsrc, ddst, dval, (int)n, (int64_t)st->unit_bytes, st->cfg.head_dim,
                      zero_tail, s, i);
     });
@@ -862,7 +873,7 @@ extern "C" hs_status hs_stage_prefill(hs_stage* st, int32_t n, const int64_t* id
   if (first) {
     r = wait_need(s, ne[0]);
     if (r != HS_OK) return r;
-    r = run(st, s, [&](LaunchInfo* i) {
+    r = run(st, s, "embed", [&](LaunchInfo* i) {
       return embed(static_cast<const int32_t*>(in), W(st, st->L.embed), st->cfg.vocab, H, (int)T,
                    x, s, i);
     });
@@ -963,7 +974,7 @@ extern "C" hs_status hs_stage_decode(hs_stage* st, int32_t n, const int64_t* ids
   if (first) {
     r = wait_need(s, ne[0]);
     if (r != HS_OK) return r;
-    r = run(st, s, [&](LaunchInfo* i) {
+    r = run(st, s, "embed", [&](LaunchInfo* i) {
       return embed(static_cast<const int32_t*>(in), W(st, st->L.embed), st->cfg.vocab, H, n, x, s, i);
     });
     if (r != HS_OK) return r;
@@ -1330,6 +1341,20 @@ extern "C" hs_status hs_stage_set_timing(hs_stage* st, int32_t enable) {
   ABI_END
 }
 
+extern "C" hs_status hs_stage_set_timing_sites(hs_stage* st, const char* sites) {
+  ABI_BEGIN
+  if (!st) return fail(HS_EINVAL, "null stage");
+  std::string list;
+  if (sites && *sites) {
+    for (const char* c = sites; *c; ++c)
+      if (*c != ' ') list.push_back(*c);
+    list = "," + list + ",";
+  }
+  st->timing_sites = list;
+  return HS_OK;
+  ABI_END
+}
+
 extern "C" hs_status hs_stage_read_timing(hs_stage* st, hs_kernel_stat* out, int32_t cap,
                                           int32_t* n) {
   ABI_BEGIN
@@ -1340,7 +1365,9 @@ extern "C" hs_status hs_stage_read_timing(hs_stage* st, hs_kernel_stat* out, int
   for (auto& p : st->pending) {
     float ms = 0;
     HIPTRY(hipEventElapsedTime(&ms, p.a, p.b));
-    Stat& s = st->stats[p.name];
+    Stat& s = st->stats[p.name + "@" + p.site];
+    s.name = p.name;
+    s.site = p.site;
     s.launches += 1;
     s.ms += ms;
     s.flops += p.flops;
@@ -1354,7 +1381,8 @@ extern "C" hs_status hs_stage_read_timing(hs_stage* st, hs_kernel_stat* out, int
     if (i < cap) {
       hs_kernel_stat& o = out[i];
       memset(&o, 0, sizeof o);
-      strncpy(o.name, kv.first.c_str(), sizeof(o.name) - 1);
+      strncpy(o.name, kv.second.name.c_str(), sizeof(o.name) - 1);
+      strncpy(o.site, kv.second.site.c_str(), sizeof(o.site) - 1);
       o.launches = kv.second.launches;
       o.total_ms = kv.second.ms;
       o.flops = kv.second.flops;

@@ -68,7 +68,8 @@ class hs_kv_blob_info(C.Structure):
 
 
 class hs_kernel_stat(C.Structure):
-    _fields_ = [("name", C.c_char * 48), ("launches", C.c_int64), ("total_ms", C.c_double),
+    _fields_ = [("name", C.c_char * 48), ("site", C.c_char * 16), ("launches", C.c_int64),
+                ("total_ms", C.c_double),
                 ("flops", C.c_double), ("bytes", C.c_double)]
 
 
@@ -99,6 +100,7 @@ _SIGS = {
     "hs_stage_merge": [_P, C.POINTER(_P), C.c_int32, _P],
     "hs_kv_blob_describe": [_P, C.c_uint64, C.POINTER(hs_kv_blob_info)],
     "hs_stage_set_timing": [_P, C.c_int32],
+    "hs_stage_set_timing_sites": [_P, C.c_char_p],
     "hs_stage_read_timing": [_P, C.POINTER(hs_kernel_stat), C.c_int32, C.POINTER(C.c_int32)],
     # single-kernel entry points (include/hs_kernel.h)
     "hs_k_gemm": [_P, C.c_int64, _P, _P, C.c_int64, _P, C.c_int64, C.c_int32, C.c_int32,
@@ -284,12 +286,20 @@ def hs_stage_set_timing(h, enable):
     _check(lib().hs_stage_set_timing(h, 1 if enable else 0))
 
 
+def hs_stage_set_timing_sites(h, sites=None):
+    """Restrict timing to the named launch sites (list or comma string; None = all)."""
+    if sites is not None and not isinstance(sites, str):
+        sites = ",".join(sites)
+    _check(lib().hs_stage_set_timing_sites(h, sites.encode() if sites else None))
+
+
 def hs_stage_read_timing(h, cap=256):
     """Per-kernel timing since the last read (waits for the stage; resets)."""
     arr = (hs_kernel_stat * cap)()
     n = C.c_int32(0)
     _check(lib().hs_stage_read_timing(h, arr, cap, C.byref(n)))
-    return [dict(name=a.name.decode(), launches=a.launches, total_ms=a.total_ms,
+    return [dict(name=a.name.decode(), site=a.site.decode(), launches=a.launches,
+                 total_ms=a.total_ms,
                  flops=a.flops, bytes=a.bytes) for a in arr[:min(n.value, cap)]]
 
 

@@ -343,3 +343,36 @@ def test_error_paths(env):
     gap = make(env, 0, 0, resident=(0, 1))
     assert code(hs.hs_stage_merge, gap.h, [st.h, s1.h], sp) == hs.HS_ESTATE  # not resident
     assert st.info()["live_seqs"] == 1
+
+
+def test_timing_sites_filter(env):
+    """Timing every site reports every kernel of the forward pass; naming
+    sites reports only their launches (one per layer), and results do not
+    depend on timing."""
+    hs = env["hs"]
+    st = make(env, 0, 2)
+    hs.hs_stage_read_timing(st.h)
+    hs.hs_stage_set_timing(st.h, 1)
+    h_all = _hidden_prefill_full(st, env["prompt"], seq_id=1)
+    all_stats = hs.hs_stage_read_timing(st.h)
+    sites = {s["site"] for s in all_stats}
+    assert {"embed", "attn_norm", "qkv", "rope_kv", "attn", "o_proj", "ffn_norm", "gate_up",
+            "down", "final_norm", "lm_head", "argmax"} <= sites
+    hs.hs_stage_set_timing_sites(st.h, "qkv, down")
+    h_two = _hidden_prefill_full(st, env["prompt"], seq_id=2)
+    two = hs.hs_stage_read_timing(st.h)
+    assert {s["site"] for s in two} == {"qkv", "down"}
+    assert all(s["launches"] == CFG.n_layers and s["total_ms"] > 0 for s in two)
+    hs.hs_stage_set_timing(st.h, 0)
+    hs.hs_stage_set_timing_sites(st.h, None)
+    assert np.array_equal(h_all, h_two)
+
+
+def _hidden_prefill_full(st, tokens, seq_id):
+    torch = G.torch()
+    x = torch.from_numpy(np.asarray(tokens, np.int32)).cuda()
+    nxt = torch.zeros(1, dtype=torch.int32, device="cuda")
+    logits = torch.zeros((1, CFG.vocab), dtype=torch.float32, device="cuda")
+    st.prefill([seq_id], [len(tokens)], x.data_ptr(), nxt.data_ptr(), logits.data_ptr(),
+               G.stream_ptr())
+    return logits.cpu().numpy()
