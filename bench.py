@@ -57,20 +57,23 @@ def log(*a):
 
 
 def traffic_from_profiles(kernel):
-    """HBM bytes per launch of `kernel` from the committed counter summary,
-    if it was taken on the current kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", "pmc_traffic.json")
-    if not os.path.exists(path):
-        return None
-    with open(path) as f:
-        rec = json.load(f)
+    """HBM bytes per launch of `kernel` from the committed counter summaries
+    (profiles/*traffic*.md, a line "traffic: kernel=K hbm_bytes_per_launch=B
+    k_gemm_sha256=H"), if they were taken on the current GEMM source; else
+    None."""
+    import glob
     src = os.path.join(ROOT, "paper_2502_15524_amd", "csrc", "k_gemm.hip")
     with open(src, "rb") as f:
         h = hashlib.sha256(f.read()).hexdigest()
-    k = rec.get("kernels", {}).get(kernel)
-    if not k or rec.get("k_gemm_sha256") != h:
-        return None
-    return k.get("hbm_bytes_per_launch")
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*traffic*.md"))):
+        with open(path) as f:
+            for line in f:
+                if not line.startswith("traffic:"):
+                    continue
+                kv = dict(t.split("=", 1) for t in line.split()[1:])
+                if kv.get("kernel") == kernel and kv.get("k_gemm_sha256") == h:
+                    return int(kv["hbm_bytes_per_launch"])
+    return None
 
 
 def cpu_baseline(wl, x_f32, stage_range, min_seconds=12.0):
