@@ -46,6 +46,11 @@ def parse():
     ap.add_argument("--chunk-mb", type=int, default=64)
     ap.add_argument("--copy-streams", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workload", default="7b-stage8-15-cold",
+                    help="7b-stage8-15-cold (default: one stage, cold TTFT) or one of "
+                         "7b-full-b8, 13b-2x20-b4, 8b-4x8-ragged-merge (whole pipeline on "
+                         "this GPU: batched prefill, decode, and for the last one KV "
+                         "export/import and merge)")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="only run a few warm prefill steps and a 256 MiB device copy "
                          "(the workload for hardware-counter passes)")
@@ -116,6 +121,8 @@ def main():
     from paper_2502_15524_amd import hs, pipeline
     from workloads import WORKLOADS, gen
 
+    if args.workload != "7b-stage8-15-cold":
+        return bench_pipeline(WORKLOADS[args.workload], args)
     wl = WORKLOADS["7b-stage8-15-cold"]
     cfg = wl.cfg
     b, e = wl.stages[wl.bench_stage]
@@ -274,6 +281,12 @@ def main():
     ev1.record(stream)
     stream.synchronize()
     dec_ms = ev0.elapsed_time(ev1) / nd
+
+    def two_decode_steps():
+        for _ in range(4):
+            st.decode([i], xd.data_ptr(), od.data_ptr(), 0, sp)
+        stream.synchronize()
+    log_decode_breakdown(hs, [st], two_decode_steps, 2)
     ctx = P + args.decode_steps
     kv_tok = 2 * cfg.n_kv_heads * cfg.head_dim * 2 * (e - b)
     dec_bytes = img.numel() + ctx * kv_tok
@@ -336,6 +349,237 @@ def main():
         "kv_import_GBps": round(2 * used / (imp_ms / 1e3) / 1e9, 1),
     }
     st.close()
+    print(json.dumps(res), flush=True)
+
+
+def log_decode_breakdown(hs, stages, run, n_steps):
+    """Run `run` with every launch of `stages` timed; log the per-kernel
+    share of the decode steps."""
+    for st in stages:
+        hs.hs_stage_read_timing(st.h)
+        hs.hs_stage_set_timing_sites(st.h, None)
+        hs.hs_stage_set_timing(st.h, 1)
+    run()
+    agg = {}
+    for st in stages:
+        hs.hs_stage_set_timing(st.h, 0)
+        for k in hs.hs_stage_read_timing(st.h):
+            a = agg.setdefault((k["name"], k["site"]), dict(k, launches=0, total_ms=0.0, bytes=0.0))
+            a["launches"] += k["launches"]
+            a["total_ms"] += k["total_ms"]
+            a["bytes"] += k["bytes"]
+    tot = sum(a["total_ms"] for a in agg.values())
+    steps = n_steps + 2      # run() includes its own two warm-up steps
+    log(f"[bench] decode breakdown (every launch timed, {tot / steps:.3f} ms of kernels/step):")
+    for a in sorted(agg.values(), key=lambda a: -a["total_ms"])[:10]:
+        avg = a["total_ms"] / a["launches"]
+        bw = (a["bytes"] / a["launches"]) / (avg / 1e3) / 1e9 if a["bytes"] else 0
+        log(f"[bench]   {a['name']:<28} {a['site']:<10} x{a['launches'] // steps:<3} avg "
+            f"{avg * 1e3:8.1f} us {100 * a['total_ms'] / tot:5.1f}%  {bw:7.0f} GB/s")
+
+
+def bench_pipeline(wl, args):
+    """A whole pipeline (every stage of the workload) on this GPU, weights
+    resident: batched prefill through all stages, greedy decode steps, and
+    for workloads that merge, KV export/import of every stage and the merge
+    into one worker holding all layers, then decode in the merged worker.
+    Prints one JSON line; `value` = prefill tok/s of the whole batch."""
+    import numpy as np
+    import torch
+    from paper_2502_15524_amd import hs, pipeline
+    from workloads import gen
+
+    cfg = wl.cfg
+    lens = wl.lengths()
+    B, T, H, V = len(lens), sum(lens), cfg.hidden, cfg.vocab
+    n_dec = min(wl.decode_steps, args.decode_steps)
+    max_ctx = max(lens) + 2 * (n_dec + 2) + 16
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.Stream()
+    sp = stream.cuda_stream
+    kv_tok_layer = 2 * cfg.n_kv_heads * cfg.head_dim * 2
+    merge = len(wl.stages) > 1 and wl.name.endswith("merge")
+
+    # With a merge, the first stage keeps every layer resident (it is the
+    # worker the others merge into); it serves only its own range until then.
+    t0 = time.perf_counter()
+    stages, img_bytes = [], 0
+    for k, (b, e) in enumerate(wl.stages):
+        rb, re = (0, cfg.n_layers) if merge and k == 0 else (b, e)
+        img = pipeline.pinned_image(cfg, rb, re)
+        st = pipeline.Stage(cfg, b, e, max_seqs=B + 2, max_ctx=max_ctx, max_batch_tokens=T,
+                            resident=(rb, re))
+        st.load(img, 64 << 20)
+        st.sync()
+        img.close()
+        img_bytes += hs.hs_weight_layout(pipeline.hs_cfg(cfg), b, e)[1]
+        stages.append(st)
+    log(f"[bench] {wl.name}: {len(stages)} stage(s) {wl.stages}, {img_bytes / 1e9:.2f} GB of "
+        f"serving weights loaded in {time.perf_counter() - t0:.1f} s; batch {B}, {T} prompt "
+        f"tokens")
+
+    toks = torch.from_numpy(gen.tokens(V, T, wl.seed)).to(dev)
+    hid = [torch.empty((T, H), dtype=torch.bfloat16, device=dev) for _ in range(2)]
+    nxt = torch.empty(B, dtype=torch.int32, device=dev)
+    ids_next = [10_000]
+
+    def prefill_all():
+        ids = list(range(ids_next[0], ids_next[0] + B))
+        ids_next[0] += B
+        x = toks
+        for i, st in enumerate(stages):
+            out = nxt if i == len(stages) - 1 else hid[i % 2]
+            st.prefill(ids, lens, x.data_ptr(), out.data_ptr(), 0, sp)
+            x = out
+        return ids
+
+    def free(ids):
+        for st in stages:
+            for i in ids:
+                hs.hs_seq_free(st.h, i)
+
+    def timed(fn, reps):
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        t0 = time.perf_counter()
+        out = [fn() for _ in range(reps)]
+        ev1.record(stream)
+        stream.synchronize()
+        return max(ev0.elapsed_time(ev1), (time.perf_counter() - t0) * 1e3) / reps, out
+
+    # prefill: one step with every launch timed (breakdown), then timed steps
+    for st in stages:
+        hs.hs_stage_read_timing(st.h)
+        hs.hs_stage_set_timing(st.h, 1)
+    free(prefill_all())
+    stream.synchronize()
+    stats = {}
+    for st in stages:
+        hs.hs_stage_set_timing(st.h, 0)
+        for k in hs.hs_stage_read_timing(st.h):
+            key = (k["name"], k["site"])
+            a = stats.setdefault(key, dict(k, launches=0, total_ms=0.0, flops=0.0))
+            a["launches"] += k["launches"]
+            a["total_ms"] += k["total_ms"]
+            a["flops"] += k["flops"]
+    kern_ms = sum(a["total_ms"] for a in stats.values())
+    flops_step = sum(a["flops"] for a in stats.values())
+    for a in sorted(stats.values(), key=lambda a: -a["total_ms"])[:8]:
+        avg = a["total_ms"] / a["launches"]
+        rate = (a["flops"] / a["launches"]) / (avg / 1e3) / 1e12 if a["flops"] else 0
+        log(f"[bench]   {a['name']:<28} {a['site']:<10} x{a['launches']:<4} avg "
+            f"{avg * 1e3:9.1f} us {100 * a['total_ms'] / kern_ms:5.1f}%  {rate:7.1f} TFLOP/s")
+    dom = max(stats.values(), key=lambda a: a["total_ms"])
+    reps = max(1, min(args.steps, 5))
+    for st in stages:
+        hs.hs_stage_set_timing_sites(st.h, dom["site"])
+        hs.hs_stage_set_timing(st.h, 1)
+    ms_pre, _ = timed(lambda: free(prefill_all()), reps)
+    timed_stats = []
+    for st in stages:
+        hs.hs_stage_set_timing(st.h, 0)
+        hs.hs_stage_set_timing_sites(st.h, None)
+        timed_stats += [k for k in hs.hs_stage_read_timing(st.h)
+                        if k["name"] == dom["name"] and k["site"] == dom["site"]]
+    d_launch = sum(k["launches"] for k in timed_stats)
+    d_avg_s = sum(k["total_ms"] for k in timed_stats) / d_launch / 1e3
+    d_flops = sum(k["flops"] for k in timed_stats) / d_launch
+    achieved = d_flops / d_avg_s / 1e12
+    log(f"[bench] prefill {ms_pre:.2f} ms = {T / ms_pre * 1e3:,.0f} tok/s "
+        f"({flops_step / (ms_pre / 1e3) / 1e12:.0f} TFLOP/s, "
+        f"{flops_step / (ms_pre / 1e3) / 1e12 / PEAK_BF16_TFLOPS:.1%} of MFMA peak); dominant "
+        f"{dom['name']} ({dom['site']}) {d_avg_s * 1e6:.1f} us, {achieved:.0f} TFLOP/s")
+
+    # decode: greedy steps through every stage
+    def decode_steps(sts, ids, n, x0):
+        x = x0
+        hbuf = [torch.empty((B, H), dtype=torch.bfloat16, device=dev) for _ in range(2)]
+
+        def one():
+            xi = x
+            for i, st in enumerate(sts):
+                out = nxt if i == len(sts) - 1 else hbuf[i % 2]
+                st.decode(ids, xi.data_ptr(), out.data_ptr(), 0, sp)
+                xi = out
+        for _ in range(2):
+            one()
+        ms, _ = timed(one, n)
+        return ms
+
+    ids = prefill_all()
+    x_tok = nxt.clone()
+    ms_dec = decode_steps(stages, ids, n_dec, x_tok)
+    log_decode_breakdown(hs, stages, lambda: decode_steps(stages, ids, 2, x_tok), 2)
+    ctx_mid = np.array(lens) + 2 + n_dec / 2.0
+    w_bytes = img_bytes - (V * H * 2) + B * H * 2   # embedding: B rows per step
+    kv_read = float(ctx_mid.sum()) * kv_tok_layer * cfg.n_layers
+    dec_bytes = w_bytes + kv_read + B * kv_tok_layer * cfg.n_layers
+    log(f"[bench] decode B={B} {ms_dec:.3f} ms/step = {B / ms_dec * 1e3:,.0f} tok/s, "
+        f"{dec_bytes / (ms_dec / 1e3) / 1e9:,.0f} GB/s "
+        f"({dec_bytes / (ms_dec / 1e3) / 1e9 / PEAK_HBM_GBPS:.1%} of HBM; weights "
+        f"{w_bytes / 1e9:.2f} GB + KV {kv_read / 1e9:.2f} GB per step)")
+    res_extra = {}
+    if merge:
+        # KV export of every stage to device blobs, and import of all of them
+        # into a fresh worker holding every layer's pools
+        blobs, exp_ms, moved = [], [], 0
+        for st in stages:
+            size = hs.hs_kv_export_size(st.h, ids)
+            blob = torch.empty(size, dtype=torch.uint8, device=dev)
+            hs.hs_kv_export(st.h, ids, blob.data_ptr(), size, sp)   # warm
+            ms, _ = timed(lambda: hs.hs_kv_export(st.h, ids, blob.data_ptr(), size, sp), 5)
+            exp_ms.append(ms)
+            blobs.append((blob, size))
+            moved += size - 256
+        tgt = pipeline.Stage(cfg, 0, cfg.n_layers, max_seqs=B + 2, max_ctx=max_ctx,
+                             max_batch_tokens=T)
+        imp_ms = []
+        for r in range(3):
+            if r:
+                for i in ids:
+                    hs.hs_seq_free(tgt.h, i)
+            ms_r, _ = timed(lambda: [hs.hs_kv_import(tgt.h, b.data_ptr(), n, sp)
+                                     for b, n in blobs], 1)
+            imp_ms.append(ms_r)
+        tgt.close()
+        ms_imp = statistics.median(imp_ms)
+        ms_exp = sum(exp_ms)
+        log(f"[bench] KV export {moved / 1e9:.2f} GB in {ms_exp:.2f} ms "
+            f"({2 * moved / (ms_exp / 1e3) / 1e9:,.0f} GB/s), import {ms_imp:.2f} ms "
+            f"({2 * moved / (ms_imp / 1e3) / 1e9:,.0f} GB/s)")
+        # the merge itself: stage 0 takes over every layer (drain, block
+        # copies into its pools, serving range extended), then decodes alone
+        ms_merge, _ = timed(lambda: hs.hs_stage_merge(stages[0].h, [st.h for st in stages[1:]],
+                                                      sp), 1)
+        ms_dec_m = decode_steps([stages[0]], ids, n_dec, x_tok)
+        log(f"[bench] merge {ms_merge:.2f} ms; merged-worker decode B={B} {ms_dec_m:.3f} "
+            f"ms/step = {B / ms_dec_m * 1e3:,.0f} tok/s")
+        res_extra = {"kv_export_ms": round(ms_exp, 3), "kv_import_ms": round(ms_imp, 3),
+                     "kv_bytes": moved,
+                     "kv_export_GBps": round(2 * moved / (ms_exp / 1e3) / 1e9, 1),
+                     "kv_import_GBps": round(2 * moved / (ms_imp / 1e3) / 1e9, 1),
+                     "merge_ms": round(ms_merge, 3),
+                     "merged_decode_ms_per_step": round(ms_dec_m, 4),
+                     "merged_decode_tok_s": round(B / ms_dec_m * 1e3, 1)}
+    res = {
+        "metric": METRIC, "value": round(T / ms_pre * 1e3, 1), "unit": "tok/s", "n_gpus": 1,
+        "steps": reps, "warmup": 1, "ms_per_step": round(ms_pre, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.name, "model_shape": cfg.name, "stages": wl.stages,
+                   "batch": B, "prompt_tokens": T, "decode_steps": n_dec},
+        "roofline": {"bound": "mfma", "kernel": dom["name"], "achieved": round(achieved, 1),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None},
+        "cpu_baseline": None,
+        "prefill_mfma_frac_step": round(flops_step / (ms_pre / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "decode_ms_per_step": round(ms_dec, 4), "decode_tok_s": round(B / ms_dec * 1e3, 1),
+        "decode_hbm_frac": round(dec_bytes / (ms_dec / 1e3) / 1e9 / PEAK_HBM_GBPS, 4),
+    }
+    res.update(res_extra)
+    for st in stages:
+        st.close()
     print(json.dumps(res), flush=True)
 
 

@@ -45,6 +45,25 @@ hs_status hs_k_attn_prefill(const void* qkv, void* out, const int32_t* cu_seqlen
                             int32_t n_seqs, int32_t n_heads, int32_t n_kv_heads,
                             int32_t head_dim, void* stream);
 
+/* Attention of one new query per sequence over its paged KV cache (the
+ * attention of a decode step: the keys and values cached during prefill and
+ * earlier steps are reused). q: bf16 [B][ldq], query head h at column
+ * h * head_dim, already rotated; pool: one layer's KV pool, bf16
+ * [blocks][K | V][n_kv_heads][16][head_dim] with post-RoPE keys;
+ * block_table: device int32 [B][max_blocks] (logical block -> pool block);
+ * ctx: device int32 [B], cached tokens of each sequence including the new
+ * one (1 <= ctx <= max_ctx); out: bf16 [B][ldo], head h at column
+ * h * head_dim. max_ctx (host) sizes the launch. The context is processed in
+ * fixed 64-token splits whose partial results go through a workspace that
+ * the library allocates per device on first use and grows when needed
+ * (calls on one device must not overlap); the call is asynchronous on
+ * `stream` and deterministic. */
+hs_status hs_k_attn_decode(const void* q, int64_t ldq, const void* pool,
+                           const int32_t* block_table, const int32_t* ctx, void* out,
+                           int64_t ldo, int32_t B, int32_t n_heads, int32_t n_kv_heads,
+                           int32_t head_dim, int32_t max_blocks, int32_t max_ctx,
+                           void* stream);
+
 /* RMSNorm of `rows` rows of width `hidden`: out = x / sqrt(mean(x^2) + eps) * g,
  * bf16 in and out, float32 arithmetic. */
 hs_status hs_k_rmsnorm(const void* x, const void* g, void* out, int32_t rows, int32_t hidden,

@@ -89,8 +89,11 @@ struct AttnDecodeArgs {
 hipError_t attn_decode(const AttnDecodeArgs& a, hipStream_t s, LaunchInfo* info_split,
                        LaunchInfo* info_combine);
 
-hipError_t argmax_rows(const float* logits, int n_rows, int n_cols, int32_t* out, hipStream_t s,
-                       LaunchInfo* info);
+// Greedy token per row: lowest index of the row's maximum. part: scratch of
+// n_rows * argmax_chunks(n_cols) * 2 int32.
+int argmax_chunks(int n_cols);
+hipError_t argmax_rows(const float* logits, int n_rows, int n_cols, int32_t* part, int32_t* out,
+                       hipStream_t s, LaunchInfo* info);
 
 // Copy `n_units` KV units (a K block followed by its V block, unit_bytes each);
 // slots at or past valid[u] are written as zero when zero_tail is set.

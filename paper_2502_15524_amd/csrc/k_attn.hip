@@ -8,6 +8,8 @@
 #include "hs_device.h"
 #include "hs_kernels.h"
 
+#include <algorithm>
+
 namespace hs {
 
 // ------------------------------------------------------------------ prefill
@@ -206,10 +208,34 @@ int attn_prefill_waves(int64_t tiles_of_128, int n_heads) {
 
 // ------------------------------------------------------------------- decode
 //
-// One workgroup per (split, kv head, sequence). D/8 lanes share a token (one
-// 16-byte chunk each), so 256 threads cover 2048/D tokens per pass; every
-// thread keeps an online softmax over its tokens for the G query heads of
-// the KV head, and the token groups are merged through LDS at the end.
+// The context of a sequence is cut into fixed 64-token splits; one
+// workgroup per (split, kv head, sequence). D/8 lanes share a token (one
+// 16-byte chunk of its key and value rows each), so 256 threads cover
+// 2048/D tokens per pass and every thread sees 4 tokens of the split. Per
+// group of 4 tokens a thread forms the G scores (partial dot products summed
+// over the token's lanes with DPP row operations), then updates its online
+// softmax once: new max, one rescale of the accumulators, four
+// probabilities. The token slots are merged through LDS in a fixed order.
+// Output per split and query head: the unnormalised P V, the max score
+// (log2 domain) and the sum of exp2(score - max); the combine kernel merges
+// the splits in order.
+
+// Sum over the 16 lanes of a DPP row (all lanes get the sum). Each step adds
+// a lane permutation that pairs lanes holding disjoint partial sums.
+__device__ __forceinline__ float row16_sum(float v) {
+  v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, true));   // quad_perm 1,0,3,2
+  v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x4E, 0xF, 0xF, true));   // quad_perm 2,3,0,1
+  v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x141, 0xF, 0xF, true));  // row_half_mirror
+  v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x140, 0xF, 0xF, true));  // row_mirror
+  return v;
+}
+// Sum over 8 lanes (lanes 8k..8k+7 of a row).
+__device__ __forceinline__ float row8_sum(float v) {
+  v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, true));
+  v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x4E, 0xF, 0xF, true));
+  v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x141, 0xF, 0xF, true));
+  return v;
+}
 
 template <int D, int G>
 __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a, float scale_log2) {
@@ -218,6 +244,7 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a
   constexpr int PASSES = kDecodeSplit / TPP;
   constexpr int UNR = PASSES < 4 ? PASSES : 4;
   static_assert(PASSES % UNR == 0, "split/pass mismatch");
+  static_assert(LPT == 16 || LPT == 8, "head dim 128 or 64");
   __shared__ float s_ml[TPP][G][2];
   __shared__ float s_acc[TPP][G][D];
 
@@ -227,7 +254,24 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a
   if (t_begin >= ctx) return;  // uniform across the workgroup
   const int tid = threadIdx.x, tl = tid / LPT, c = tid % LPT;
   const int h0 = kh * G;
+  const int32_t* bt = a.block_table + (int64_t)b * a.max_blocks;
+  const int64_t kv_stride = (int64_t)a.n_kv_heads * 16 * D;  // K block -> V block
 
+  // all key and value loads of the split go out first
+  pack8 kv[PASSES], vv[PASSES];
+#pragma unroll
+  for (int p = 0; p < PASSES; ++p) {
+    const int tok = t_begin + p * TPP + tl;
+    kv[p] = zero8();
+    vv[p] = zero8();
+    if (tok < ctx) {
+      const int phys = bt[tok >> 4];
+      const bf16_t* kp = a.pool + ((int64_t)phys * 2 * a.n_kv_heads + kh) * 16 * D +
+                         (tok & 15) * D + c * 8;
+      kv[p] = ld16(kp);
+      vv[p] = ld16(kp + kv_stride);
+    }
+  }
   float q[G][8];
 #pragma unroll
   for (int gg = 0; gg < G; ++gg) {
@@ -238,108 +282,119 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a
       q[gg][2 * e + 1] = hi_bf(v.w[e]);
     }
   }
-  float m[G], l[G], acc[G][8];
-#pragma unroll
-  for (int gg = 0; gg < G; ++gg) {
-    m[gg] = -INFINITY;
-    l[gg] = 0.f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[gg][e] = 0.f;
-  }
 
-  const int32_t* bt = a.block_table + (int64_t)b * a.max_blocks;
-  const int64_t kv_stride = (int64_t)a.n_kv_heads * 16 * D;  // K block -> V block
-  for (int p0 = 0; p0 < PASSES; p0 += UNR) {
-    pack8 kv[UNR], vv[UNR];
-    bool ok[UNR];
+  {
+    float m[G], l[G], acc[G][8];
 #pragma unroll
-    for (int u = 0; u < UNR; ++u) {
-      const int tok = t_begin + (p0 + u) * TPP + tl;
-      ok[u] = tok < ctx;
-      kv[u] = zero8();
-      vv[u] = zero8();
-      if (ok[u]) {
-        const int phys = bt[tok >> 4];
-        const bf16_t* kp = a.pool + ((int64_t)phys * 2 * a.n_kv_heads + kh) * 16 * D +
-                           (tok & 15) * D + c * 8;
-        kv[u] = ld16(kp);
-        vv[u] = ld16(kp + kv_stride);
-      }
+    for (int gg = 0; gg < G; ++gg) {
+      m[gg] = -INFINITY;
+      l[gg] = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[gg][e] = 0.f;
     }
 #pragma unroll
-    for (int u = 0; u < UNR; ++u) {
-      float kf[8], vf[8];
+    for (int p0 = 0; p0 < PASSES; p0 += UNR) {
+      float sc[UNR][G];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        kf[2 * e] = lo_bf(kv[u].w[e]);
-        kf[2 * e + 1] = hi_bf(kv[u].w[e]);
-        vf[2 * e] = lo_bf(vv[u].w[e]);
-        vf[2 * e + 1] = hi_bf(vv[u].w[e]);
+      for (int u = 0; u < UNR; ++u) {
+        const bool ok = t_begin + (p0 + u) * TPP + tl < ctx;
+        float kf[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          kf[2 * e] = lo_bf(kv[p0 + u].w[e]);
+          kf[2 * e + 1] = hi_bf(kv[p0 + u].w[e]);
+        }
+#pragma unroll
+        for (int gg = 0; gg < G; ++gg) {
+          float d = 0.f;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) d += q[gg][e] * kf[e];
+          d = LPT == 16 ? row16_sum(d) : row8_sum(d);
+          sc[u][gg] = ok ? d * scale_log2 : -INFINITY;
+        }
       }
 #pragma unroll
       for (int gg = 0; gg < G; ++gg) {
-        float sc = 0.f;
+        float mx = m[gg];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) sc += q[gg][e] * kf[e];
+        for (int u = 0; u < UNR; ++u) mx = fmaxf(mx, sc[u][gg]);
+        if (mx == -INFINITY) continue;  // no valid token yet for this slot
+        const float corr = fast_exp2(m[gg] - mx);
+        l[gg] *= corr;
 #pragma unroll
-        for (int o = LPT / 2; o > 0; o >>= 1) sc += __shfl_xor(sc, o, 64);
-        if (ok[u]) {
-          const float s2 = sc * scale_log2;
-          const float mn = fmaxf(m[gg], s2);
-          const float corr = fast_exp2(m[gg] - mn);
-          const float pr = fast_exp2(s2 - mn);
-          m[gg] = mn;
-          l[gg] = l[gg] * corr + pr;
+        for (int e = 0; e < 8; ++e) acc[gg][e] *= corr;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) acc[gg][e] = acc[gg][e] * corr + pr * vf[e];
+        for (int u = 0; u < UNR; ++u) {
+          const float pr = sc[u][gg] == -INFINITY ? 0.f : fast_exp2(sc[u][gg] - mx);
+          l[gg] += pr;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            acc[gg][2 * e] += pr * lo_bf(vv[p0 + u].w[e]);
+            acc[gg][2 * e + 1] += pr * hi_bf(vv[p0 + u].w[e]);
+          }
         }
+        m[gg] = mx;
       }
     }
-  }
 
 #pragma unroll
-  for (int gg = 0; gg < G; ++gg) {
+    for (int gg = 0; gg < G; ++gg) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) s_acc[tl][gg][c * 8 + e] = acc[gg][e];
-    if (c == 0) {
-      s_ml[tl][gg][0] = m[gg];
-      s_ml[tl][gg][1] = l[gg];
+      for (int e = 0; e < 8; ++e) s_acc[tl][gg][c * 8 + e] = acc[gg][e];
+      if (c == 0) {
+        s_ml[tl][gg][0] = m[gg];
+        s_ml[tl][gg][1] = l[gg];
+      }
     }
-  }
-  __syncthreads();
-  for (int i = tid; i < G * D; i += 256) {
-    const int gg = i / D, d = i % D;
-    float M = -INFINITY;
-    for (int t = 0; t < TPP; ++t) M = fmaxf(M, s_ml[t][gg][0]);
-    float L = 0.f, O = 0.f;
-    for (int t = 0; t < TPP; ++t) {
-      const float mt = s_ml[t][gg][0];
-      if (mt == -INFINITY) continue;
-      const float w = fast_exp2(mt - M);
-      L += s_ml[t][gg][1] * w;
-      O += s_acc[t][gg][d] * w;
-    }
-    const int64_t idx = ((int64_t)b * a.n_heads + h0 + gg) * a.max_splits + split;
-    a.part_o[idx * D + d] = O;
-    if (d == 0) {
-      a.part_ml[idx * 2] = M;
-      a.part_ml[idx * 2 + 1] = L;
+    __syncthreads();
+    for (int i = tid; i < G * D; i += 256) {
+      const int gg = i / D, d = i % D;
+      float M = -INFINITY;
+      for (int t = 0; t < TPP; ++t) M = fmaxf(M, s_ml[t][gg][0]);
+      float L = 0.f, O = 0.f;
+      for (int t = 0; t < TPP; ++t) {
+        const float mt = s_ml[t][gg][0];
+        if (mt == -INFINITY) continue;
+        const float w = fast_exp2(mt - M);
+        L += s_ml[t][gg][1] * w;
+        O += s_acc[t][gg][d] * w;
+      }
+      const int64_t idx = ((int64_t)b * a.n_heads + h0 + gg) * a.max_splits + split;
+      a.part_o[idx * D + d] = O;
+      if (d == 0) {
+        a.part_ml[idx * 2] = M;
+        a.part_ml[idx * 2 + 1] = L;
+      }
     }
   }
 }
 
+// Merge the splits of one (head, sequence) in split order with a running
+// max; the partials of 8 splits are loaded together.
 template <int D>
 __global__ __launch_bounds__(D) void attn_decode_combine_kernel(AttnDecodeArgs a) {
   const int h = blockIdx.x, b = blockIdx.y, d = threadIdx.x;
   const int n_splits = (a.ctx[b] + kDecodeSplit - 1) / kDecodeSplit;
   const int64_t base = ((int64_t)b * a.n_heads + h) * a.max_splits;
-  float M = -INFINITY;
-  for (int sp = 0; sp < n_splits; ++sp) M = fmaxf(M, a.part_ml[(base + sp) * 2]);
-  float L = 0.f, O = 0.f;
-  for (int sp = 0; sp < n_splits; ++sp) {
-    const float w = fast_exp2(a.part_ml[(base + sp) * 2] - M);
-    L += a.part_ml[(base + sp) * 2 + 1] * w;
-    O += a.part_o[(base + sp) * D + d] * w;
+  float M = -INFINITY, L = 0.f, O = 0.f;
+  for (int s0 = 0; s0 < n_splits; s0 += 8) {
+    float ms[8], ls[8], os[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const bool ok = s0 + u < n_splits;
+      ms[u] = ok ? a.part_ml[(base + s0 + u) * 2] : -INFINITY;
+      ls[u] = ok ? a.part_ml[(base + s0 + u) * 2 + 1] : 0.f;
+      os[u] = ok ? a.part_o[(base + s0 + u) * D + d] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (ms[u] == -INFINITY) continue;
+      const float mn = fmaxf(M, ms[u]);
+      const float wo = fast_exp2(M - mn), wn = fast_exp2(ms[u] - mn);
+      O = O * wo + os[u] * wn;
+      L = L * wo + ls[u] * wn;
+      M = mn;
+    }
   }
   a.out[(int64_t)b * a.ldo + h * D + d] = f2bf(O / L);
 }

@@ -163,19 +163,49 @@ __device__ __forceinline__ void better(float& v, int& i, float v2, int i2) {
   }
 }
 
-__global__ __launch_bounds__(256) void argmax_kernel(const float* logits, int n_cols, int32_t* out) {
-  __shared__ float sv[4];
-  __shared__ int si[4];
-  const float* row = logits + (int64_t)blockIdx.x * n_cols;
-  float bv = -INFINITY;
-  int bi = 0x7FFFFFFF;
-  for (int c = threadIdx.x; c < n_cols; c += 256) better(bv, bi, row[c], c);
+// Two passes: workgroups of the first take 4096-column chunks of a row (four
+// 16-byte loads per thread, all in flight together) and leave the chunk's
+// best (value, index); the second reduces a row's chunks in chunk order.
+// Ties go to the lowest index in both, so the result is the row's lowest
+// index of the maximum.
+constexpr int kArgmaxChunk = 4096;
+
+__device__ __forceinline__ void wave_best(float& bv, int& bi) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
     const float v2 = __shfl_xor(bv, o, 64);
     const int i2 = __shfl_xor(bi, o, 64);
     better(bv, bi, v2, i2);
   }
+}
+
+__global__ __launch_bounds__(256) void argmax_chunk_kernel(const float* logits, int n_cols,
+                                                           int n_chunks, int32_t* part) {
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  const int chunk = blockIdx.x, row = blockIdx.y;
+  const float* r = logits + (int64_t)row * n_cols;
+  const int c0 = chunk * kArgmaxChunk + threadIdx.x * 4;
+  float4 v[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int c = c0 + u * 1024;
+    v[u] = c < n_cols ? *reinterpret_cast<const float4*>(r + c)
+                      : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+  }
+  float bv = -INFINITY;
+  int bi = 0x7FFFFFFF;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int c = c0 + u * 1024;
+    if (c < n_cols) {
+      better(bv, bi, v[u].x, c);
+      better(bv, bi, v[u].y, c + 1);
+      better(bv, bi, v[u].z, c + 2);
+      better(bv, bi, v[u].w, c + 3);
+    }
+  }
+  wave_best(bv, bi);
   if ((threadIdx.x & 63) == 0) {
     sv[threadIdx.x >> 6] = bv;
     si[threadIdx.x >> 6] = bi;
@@ -183,14 +213,35 @@ __global__ __launch_bounds__(256) void argmax_kernel(const float* logits, int n_
   __syncthreads();
   if (threadIdx.x == 0) {
     for (int w = 1; w < 4; ++w) better(bv, bi, sv[w], si[w]);
-    out[blockIdx.x] = bi;
+    int32_t* o = part + ((int64_t)row * n_chunks + chunk) * 2;
+    o[0] = __float_as_int(bv);
+    o[1] = bi;
   }
 }
 
-hipError_t argmax_rows(const float* logits, int n_rows, int n_cols, int32_t* out, hipStream_t s,
-                       LaunchInfo* info) {
+__global__ __launch_bounds__(64) void argmax_final_kernel(const int32_t* part, int n_chunks,
+                                                          int32_t* out) {
+  const int row = blockIdx.x;
+  float bv = -INFINITY;
+  int bi = 0x7FFFFFFF;
+  for (int c = threadIdx.x; c < n_chunks; c += 64) {
+    const int32_t* p = part + ((int64_t)row * n_chunks + c) * 2;
+    better(bv, bi, __int_as_float(p[0]), p[1]);
+  }
+  wave_best(bv, bi);
+  if (threadIdx.x == 0) out[row] = bi;
+}
+
+int argmax_chunks(int n_cols) { return (n_cols + kArgmaxChunk - 1) / kArgmaxChunk; }
+
+hipError_t argmax_rows(const float* logits, int n_rows, int n_cols, int32_t* part, int32_t* out,
+                       hipStream_t s, LaunchInfo* info) {
   if (n_rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(argmax_kernel, dim3(n_rows), dim3(256), 0, s, logits, n_cols, out);
+  if (n_cols <= 0 || (n_cols % 4) || !part) return hipErrorInvalidValue;
+  const int nc = argmax_chunks(n_cols);
+  hipLaunchKernelGGL(argmax_chunk_kernel, dim3(nc, n_rows), dim3(256), 0, s, logits, n_cols, nc,
+                     part);
+  hipLaunchKernelGGL(argmax_final_kernel, dim3(n_rows), dim3(64), 0, s, part, nc, out);
   if (info) *info = LaunchInfo{"argmax", 0, 4.0 * n_rows * (double)n_cols};
   return hipGetLastError();
 }
@@ -199,35 +250,42 @@ hipError_t argmax_rows(const float* logits, int n_rows, int n_cols, int32_t* out
 //
 // A unit is one KV block of one layer: the K block [n_kv][16][D] followed by
 // the V block, contiguous both in the pools and in the blob. Each workgroup
-// copies up to 16 KiB of one unit with 16-byte loads and stores.
+// copies up to 16 KiB of one unit: four 16-byte loads per thread issued
+// together, then the four stores. Row r of a unit (D * 2 bytes, a power of
+// two) holds token slot r % 16.
 
 constexpr int kCopyBytesPerWg = 16384;
 
 __global__ __launch_bounds__(256) void kv_copy_kernel(const uint64_t* src, const uint64_t* dst,
                                                       const int32_t* valid, int64_t unit_bytes,
-                                                      int D, int zero_tail) {
+                                                      int row_shift, int zero_tail) {
   const int u = blockIdx.x;
   const char* s = reinterpret_cast<const char*>(src[u]);
   char* d = reinterpret_cast<char*>(dst[u]);
-  const int v = valid[u];
-  const int64_t begin = (int64_t)blockIdx.y * kCopyBytesPerWg;
-  const int64_t end = min(unit_bytes, begin + kCopyBytesPerWg);
-  const int64_t row_bytes = (int64_t)D * 2;
-  for (int64_t o = begin + threadIdx.x * 16; o < end; o += 256 * 16) {
-    const int slot = (int)((o / row_bytes) & 15);
-    pack8 x = zero8();
-    if (!zero_tail || slot < v) x = ld16(s + o);
-    st16(d + o, x);
+  const int v = zero_tail ? valid[u] : 16;
+  const int64_t begin = (int64_t)blockIdx.y * kCopyBytesPerWg + threadIdx.x * 16;
+  pack8 x[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int64_t o = begin + k * 4096;
+    const int slot = (int)((o >> row_shift) & 15);
+    x[k] = (o < unit_bytes && slot < v) ? ld16(s + o) : zero8();
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int64_t o = begin + k * 4096;
+    if (o < unit_bytes) st16(d + o, x[k]);
   }
 }
 
 hipError_t kv_copy(const uint64_t* src, const uint64_t* dst, const int32_t* valid, int n_units,
                    int64_t unit_bytes, int D, int zero_tail, hipStream_t s, LaunchInfo* info) {
   if (n_units <= 0) return hipSuccess;
-  if ((unit_bytes % 16) || (D % 8)) return hipErrorInvalidValue;
+  if ((unit_bytes % 16) || (D != 64 && D != 128)) return hipErrorInvalidValue;
   const int parts = (int)((unit_bytes + kCopyBytesPerWg - 1) / kCopyBytesPerWg);
+  const int row_shift = D == 128 ? 8 : 7;
   hipLaunchKernelGGL(kv_copy_kernel, dim3(n_units, parts), dim3(256), 0, s, src, dst, valid,
-                     unit_bytes, D, zero_tail);
+                     unit_bytes, row_shift, zero_tail);
   if (info) *info = LaunchInfo{"kv_copy", 0, 2.0 * n_units * (double)unit_bytes};
   return hipGetLastError();
 }

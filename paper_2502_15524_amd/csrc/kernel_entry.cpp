@@ -113,6 +113,53 @@ extern "C" hs_status hs_k_attn_prefill(const void* qkv, void* out, const int32_t
   }
 }
 
+namespace {
+// Split partials of hs_k_attn_decode, one buffer per device, grown on demand.
+struct DecodeWs {
+  float* buf = nullptr;
+  int64_t floats = 0;
+};
+}  // namespace
+
+extern "C" hs_status hs_k_attn_decode(const void* q, int64_t ldq, const void* pool,
+                                      const int32_t* block_table, const int32_t* ctx, void* out,
+                                      int64_t ldo, int32_t B, int32_t n_heads, int32_t n_kv_heads,
+                                      int32_t head_dim, int32_t max_blocks, int32_t max_ctx,
+                                      void* stream) {
+  try {
+    if (!q || !pool || !block_table || !ctx || !out || B < 1 || max_ctx < 1)
+      return fail(HS_EINVAL, "bad arguments");
+    if (n_kv_heads < 1 || n_heads % n_kv_heads) return fail(HS_EINVAL, "bad head counts");
+    if (max_blocks < (max_ctx + 15) / 16) return fail(HS_EINVAL, "block table too narrow");
+    static DecodeWs ws[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+      return fail(HS_EHIP, "hipGetDevice failed");
+    const int max_splits = (max_ctx + kDecodeSplit - 1) / kDecodeSplit;
+    const int64_t need = (int64_t)B * n_heads * max_splits * (head_dim + 2);
+    DecodeWs& w = ws[dev];
+    if (w.floats < need) {
+      if (w.buf) {
+        (void)hipDeviceSynchronize();
+        (void)hipFree(w.buf);
+        w.buf = nullptr;
+        w.floats = 0;
+      }
+      if (hipMalloc(reinterpret_cast<void**>(&w.buf), need * sizeof(float)) != hipSuccess)
+        return fail(HS_ENOMEM, "attention workspace");
+      w.floats = need;
+    }
+    AttnDecodeArgs a{static_cast<const bf16_t*>(q), ldq, static_cast<const bf16_t*>(pool),
+                     block_table, ctx, w.buf, w.buf + (int64_t)B * n_heads * max_splits * head_dim,
+                     static_cast<bf16_t*>(out), ldo, B, n_heads, n_kv_heads, head_dim, max_blocks,
+                     max_splits, max_splits, 0.0};
+    return launched(attn_decode(a, static_cast<hipStream_t>(stream), nullptr, nullptr),
+                    "attn_decode");
+  } catch (...) {
+    return fail(HS_EINVAL, "unexpected internal error");
+  }
+}
+
 extern "C" hs_status hs_k_rmsnorm(const void* x, const void* g, void* out, int32_t rows,
                                   int32_t hidden, float eps, void* stream) {
   try {

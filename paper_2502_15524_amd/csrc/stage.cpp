@@ -103,6 +103,7 @@ struct hs_stage {
   bf16_t *w_x = nullptr, *w_u = nullptr, *w_qkv = nullptr, *w_attn = nullptr, *w_act = nullptr,
          *w_last = nullptr;
   float *w_logits = nullptr, *w_part_o = nullptr, *w_part_ml = nullptr;
+  int32_t* w_argmax = nullptr;    // per-chunk partial results of the greedy argmax
   float* w_gpart = nullptr;       // split-k partial tiles of the projection GEMMs
   uint32_t* w_gflags = nullptr;   // their per-tile arrival counters (kept at zero)
   int64_t gpart_floats = 0, gflags_n = 0;
@@ -451,7 +452,9 @@ hs_status head_forward(hs_stage* st, const bf16_t* x, const int32_t* rows, int n
     return gemm(g, EPI_F32, s, i);
   });
   if (r != HS_OK) return r;
-  return run(st, s, "argmax", [&](LaunchInfo* i) { return argmax_rows(lg, n, m.vocab, out, s, i); });
+  return run(st, s, "argmax", [&](LaunchInfo* i) {
+    return argmax_rows(lg, n, m.vocab, st->w_argmax, out, s, i);
+  });
 }
 
 bool is_device_ptr(const void* p) {
@@ -622,7 +625,7 @@ extern "C" hs_status hs_stage_create(const hs_model_cfg* cfg, int32_t layer_begi
   for (uint64_t sz : {R * H * 2, R * H * 2, R * NQKV * 2, R * QD * 2, R * round64(F) * 2, S * H * 2,
                       S * V * 4, S * m.n_heads * st->max_splits * (uint64_t)D * 4,
                       S * m.n_heads * st->max_splits * 2 * 4, (uint64_t)st->gpart_floats * 4,
-                      (uint64_t)st->gflags_n * 4}) {
+                      (uint64_t)st->gflags_n * 4, S * (uint64_t)argmax_chunks(V) * 8}) {
     offs.push_back(off);
     off = al(off + sz);
   }
@@ -642,6 +645,7 @@ extern "C" hs_status hs_stage_create(const hs_model_cfg* cfg, int32_t layer_begi
   st->w_part_ml = reinterpret_cast<float*>(st->d_ws + offs[8]);
   st->w_gpart = st->gpart_floats ? reinterpret_cast<float*>(st->d_ws + offs[9]) : nullptr;
   st->w_gflags = st->gflags_n ? reinterpret_cast<uint32_t*>(st->d_ws + offs[10]) : nullptr;
+  st->w_argmax = reinterpret_cast<int32_t*>(st->d_ws + offs[11]);
 
   // RoPE table: angle pos * base^(-2i/D) in double, stored as float.
   {
@@ -990,6 +994,7 @@ extern "C" hs_status hs_stage_decode(hs_stage* st, int32_t n, const int64_t* ids
   c.ctx = d_ctx;
   c.call_splits = call_splits;
   c.kv_read_bytes = kv_bytes;
+
   for (int l = st->begin; l < st->end; ++l) {
     r = wait_need(s, nl[l - st->begin]);
     if (r != HS_OK) return r;

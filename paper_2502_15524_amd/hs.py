@@ -109,6 +109,8 @@ _SIGS = {
     "hs_k_attn_prefill": [_P, _P, C.POINTER(C.c_int32), C.c_int32, C.c_int32, C.c_int32,
                           C.c_int32, _P],
     "hs_k_rmsnorm": [_P, _P, _P, C.c_int32, C.c_int32, C.c_float, _P],
+    "hs_k_attn_decode": [_P, C.c_int64, _P, _P, _P, _P, C.c_int64, C.c_int32, C.c_int32,
+                         C.c_int32, C.c_int32, C.c_int32, C.c_int32, _P],
 }
 EXPORTED = sorted(list(_SIGS) + ["hs_last_error"])
 
@@ -323,6 +325,13 @@ def hs_k_attn_prefill(qkv, out, cu_seqlens, n_heads, n_kv_heads, head_dim, strea
     cu = _i32(cu_seqlens)
     _check(lib().hs_k_attn_prefill(qkv, out, cu, len(cu_seqlens) - 1, n_heads, n_kv_heads,
                                    head_dim, stream or None))
+
+
+def hs_k_attn_decode(q, ldq, pool, block_table, ctx, out, ldo, B, n_heads, n_kv_heads,
+                     head_dim, max_blocks, max_ctx, stream=0):
+    """Decode attention over a paged KV pool; block_table and ctx are device pointers."""
+    _check(lib().hs_k_attn_decode(q, ldq, pool, block_table, ctx, out, ldo, B, n_heads,
+                                  n_kv_heads, head_dim, max_blocks, max_ctx, stream or None))
 
 
 def hs_k_rmsnorm(x, g, out, rows, hidden, eps, stream=0):

@@ -144,6 +144,64 @@ def test_attn_prefill_value_ones_gives_ones():
     assert np.max(np.abs(got - 1.0)) <= 2 ** -7
 
 
+def _paged_case(lens, nh, nkv, d, seed):
+    """Random post-RoPE keys/values of ragged sequences scattered over a KV
+    pool [blocks][K|V][nkv][16][d] in a shuffled block order."""
+    rng = np.random.default_rng(seed)
+    nblk = [-(-n // 16) for n in lens]
+    total = sum(nblk) + 3
+    perm = rng.permutation(total)
+    pool = np.zeros((total, 2, nkv, 16, d), np.float32)
+    mb = max(nblk)
+    table = np.zeros((len(lens), mb), np.int32)
+    ks, vs = [], []
+    nxt = 0
+    for i, n in enumerate(lens):
+        k = gen.round_to_bf16((rng.standard_normal((n, nkv, d)) * 1.5).astype(np.float32))
+        v = gen.round_to_bf16(rng.standard_normal((n, nkv, d)).astype(np.float32))
+        ks.append(k)
+        vs.append(v)
+        for bi in range(nblk[i]):
+            phys = perm[nxt]
+            nxt += 1
+            table[i, bi] = phys
+            seg = slice(bi * 16, min(n, bi * 16 + 16))
+            cnt = seg.stop - seg.start
+            pool[phys, 0, :, :cnt] = k[seg].transpose(1, 0, 2)
+            pool[phys, 1, :, :cnt] = v[seg].transpose(1, 0, 2)
+    q = gen.round_to_bf16((rng.standard_normal((len(lens), nh * d)) * 1.5).astype(np.float32))
+    return q, pool, table, ks, vs
+
+
+@pytest.mark.parametrize("lens,nh,nkv,d", [
+    ([1], 4, 4, 64), ([17, 300, 64, 65], 4, 4, 64), ([5, 130, 1100, 64, 2100], 32, 8, 128),
+    ([512], 32, 32, 128), ([2, 129, 700], 8, 2, 128), ([1000, 33], 16, 4, 64)])
+def test_attn_decode(lens, nh, nkv, d):
+    """One query per sequence (at position ctx - 1) over a paged cache, against
+    the oracle's attention; a second call gives the same bits."""
+    torch = G.torch()
+    hs = _hs()
+    q, pool, table, ks, vs = _paged_case(lens, nh, nkv, d, sum(lens) + nh)
+    dq = G.to_dev_bf16(q)
+    dpool = G.to_dev_bf16(pool.reshape(-1))
+    dtab = torch.from_numpy(table).cuda()
+    dctx = torch.tensor(lens, dtype=torch.int32).cuda()
+    outs = []
+    for _ in range(2):
+        out = torch.zeros((len(lens), nh * d), dtype=torch.bfloat16, device="cuda")
+        hs.hs_k_attn_decode(dq.data_ptr(), nh * d, dpool.data_ptr(), dtab.data_ptr(),
+                            dctx.data_ptr(), out.data_ptr(), nh * d, len(lens), nh, nkv, d,
+                            table.shape[1], max(lens), G.stream_ptr())
+        torch.cuda.synchronize()
+        outs.append(G.from_dev_bf16(out))
+    assert np.array_equal(outs[0], outs[1])
+    for i, n in enumerate(lens):
+        ref = attention(q[i].reshape(1, nh, d).astype(np.float64), ks[i].astype(np.float64),
+                        vs[i].astype(np.float64), [n - 1], np.arange(n))[0]
+        err = np.abs(outs[0][i] - ref).max()
+        assert err <= 2e-2 * np.abs(ref).max() + 1e-3, (i, err)
+
+
 @pytest.mark.parametrize("rows,hidden", [(1, 256), (37, 4096), (5, 5120), (3, 8192)])
 def test_rmsnorm(rows, hidden):
     torch = G.torch()
