@@ -88,13 +88,17 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_kernel(AttnPrefillArgs a
       uint32_t pw[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) pw[e] = __shfl_xor(vreg[p].w[e], CPK, 64);
-      const bool odd = key & 1;
+      // selections by bit mask (all ones for an odd key): with a ternary the
+      // compiler turns the pick into a runtime index into scratch memory
+      const uint32_t odd = 0u - (uint32_t)(key & 1);
       const int kp = key >> 1;
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
-        const uint32_t mine = vreg[p].w[odd ? 2 + e : e], other = pw[odd ? 2 + e : e];
-        const uint32_t ev = odd ? other : mine, od = odd ? mine : other;  // even, odd key
-        const int col = lcol + (odd ? 4 : 0) + 2 * e;
+        const uint32_t mine = vreg[p].w[e] ^ ((vreg[p].w[e] ^ vreg[p].w[2 + e]) & odd);
+        const uint32_t other = pw[e] ^ ((pw[e] ^ pw[2 + e]) & odd);
+        const uint32_t ev = mine ^ ((mine ^ other) & odd);   // even key's word
+        const uint32_t od = other ^ ((other ^ mine) & odd);  // odd key's word
+        const int col = lcol + (key & 1) * 4 + 2 * e;
         sVt[(col) * (LV / 2) + kp] = (ev & 0xFFFFu) | (od << 16);
         sVt[(col + 1) * (LV / 2) + kp] = (ev >> 16) | (od & 0xFFFF0000u);
       }
