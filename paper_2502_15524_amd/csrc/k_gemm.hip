@@ -131,25 +131,35 @@ __device__ __forceinline__ int chunk_pos(int r, int c) {
 // pipelined against the MFMAs and the order is pinned with scheduling group
 // barriers: the A fragment of row tile i+1 is read while the TM MFMAs of row
 // tile i run, and the B fragments of the next 32-k step are read during the
-// last row tile of the current one.
+// last row tile of the current one. The last row tile of a stage is deferred
+// past the workgroup barrier: it runs while the next stage's first fragments
+// come from LDS (its operands are already in registers).
 template <int CPR>
 __device__ __forceinline__ bf16x8_v lds_frag(const bf16_t* s, int r, int c) {
   return as_bf16x8(ld16(s + (r * CPR + chunk_pos<CPR>(r, c)) * 8));
 }
 
 template <int BN, int BM, int BK, int NS, int TN, int TM, typename Dma>
-__device__ __forceinline__ void ring_stage(f32x4_v (&acc)[TN][TM], const bf16_t* sw,
+__device__ __forceinline__ void ring_stage(f32x4_v (&acc)[TN][TM], bf16x8_v (&a)[2],
+                                           bf16x8_v (&b)[2][TM], const bf16_t* sw,
                                            const bf16_t* sx, int wn, int wm, int fr, int g,
-                                           Dma&& dma) {
+                                           bool pending, Dma&& dma) {
   using T = RTile<BN, BM, BK, NS>;
   constexpr int CPR = T::CPR, KS = BK / 32;
   constexpr int MASK_MFMA = 0x008, MASK_DS_READ = 0x100;
-  bf16x8_v b[2][TM];
-  bf16x8_v a[2];
+  static_assert(TN % 2 == 0 && KS == 2, "the deferred row tile uses a[1] and b[1]");
 #pragma unroll
   for (int j = 0; j < TM; ++j) b[0][j] = lds_frag<CPR>(sx, wm * T::WM + j * 16 + fr, g);
   a[0] = lds_frag<CPR>(sw, wn * T::WN + fr, g);
   __builtin_amdgcn_sched_group_barrier(MASK_DS_READ, TM + 1, 0);
+  // the previous stage's last row tile (operands in registers) runs while
+  // this stage's first fragments are on their way from LDS
+  if (pending) {
+#pragma unroll
+    for (int j = 0; j < TM; ++j)
+      acc[TN - 1][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[1], b[1][j], acc[TN - 1][j], 0, 0, 0);
+    __builtin_amdgcn_sched_group_barrier(MASK_MFMA, TM, 0);
+  }
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
     const int c = ks * 4 + g;
@@ -165,6 +175,7 @@ __device__ __forceinline__ void ring_stage(f32x4_v (&acc)[TN][TM], const bf16_t*
           b[(ks + 1) & 1][j] = lds_frag<CPR>(sx, wm * T::WM + j * 16 + fr, c + 4);
         a[nxt] = lds_frag<CPR>(sw, wn * T::WN + fr, c + 4);
       }
+      if (ks + 1 == KS && i + 1 == TN) break;  // deferred to the next stage (or the end)
 #pragma unroll
       for (int j = 0; j < TM; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[cur], b[ks & 1][j], acc[i][j], 0, 0, 0);
@@ -280,18 +291,23 @@ void gemm_ring(GemmArgs a, GemmSched sc) {
     if (n >= NS - 1) wait_vm<(NS - 2) * LPS>();
     else wait_vm<0>();
     wg_barrier();
+    bf16x8_v fa[2], fb[2][TM];
     for (int j = 0; j < n; ++j) {
       const int stage = j % NS, nst = (j + NS - 1) % NS, kn = k0 + j + NS - 1;
       const bool more = j + NS - 1 < n;
       const bf16_t* sw = reinterpret_cast<const bf16_t*>(smem + stage * T::STAGE);
       const bf16_t* sx = reinterpret_cast<const bf16_t*>(smem + stage * T::STAGE + T::W_BYTES);
-      ring_stage<BN, BM, BK, NS>(acc, sw, sx, wn, wm, fr, g, [&](int step) {
+      ring_stage<BN, BM, BK, NS>(acc, fa, fb, sw, sx, wn, wm, fr, g, j > 0, [&](int step) {
         if (more) issue_part(nst, kn, step);
       });
       if (more) wait_vm<(NS - 2) * LPS>();
       else wait_vm<0>();
       wg_barrier();
     }
+    // the last stage's deferred row tile
+#pragma unroll
+    for (int jj = 0; jj < TM; ++jj)
+      acc[TN - 1][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[1], fb[1][jj], acc[TN - 1][jj], 0, 0, 0);
   };
 
   auto epilogue = [&](int n0, int m0) {
@@ -556,17 +572,15 @@ struct RingCfg {
   int bn, bm;
   bool sk_ok;  // has a stream-K build
 };
-const RingCfg kRing[] = {{"256x256", 256, 256, false}, {"256x256e", 256, 256, false},
-                         {"256x128", 256, 128, true}, {"128x128", 128, 128, true}};
+const RingCfg kRing[] = {{"256x256", 256, 256, false}, {"256x128", 256, 128, true},
+                         {"128x128", 128, 128, true}};
 
-// 256 x 256: 2 stages (128 KiB of LDS); "e" issues the next stage's loads
-// in the first 3/4 of the current one. 256 x 128: 3 stages. 128 x 128: 4.
+// 256 x 256: 2 stages (128 KiB of LDS), the next stage's loads issued in the
+// first half of the current one's multiplication. 256 x 128: 3 stages,
+// loads spread over the whole step. 128 x 128: 4 stages.
 hipError_t launch_ring(const RingCfg& c, const GemmArgs& a, int epi, const GemmSched& sc,
                        int grid, hipStream_t s) {
-  if (c.bn == 256 && c.bm == 256) {
-    if (c.name[7] == 'e') return dispatch_ring<256, 256, 2, 3, false>(a, epi, sc, grid, s);
-    return dispatch_ring<256, 256, 2, 4, false>(a, epi, sc, grid, s);
-  }
+  if (c.bn == 256 && c.bm == 256) return dispatch_ring<256, 256, 2, 2, false>(a, epi, sc, grid, s);
   if (c.bn == 256 && c.bm == 128)
     return sc.sk ? dispatch_ring<256, 128, 3, 4, true>(a, epi, sc, grid, s)
                  : dispatch_ring<256, 128, 3, 4, false>(a, epi, sc, grid, s);
@@ -649,8 +663,8 @@ hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info) {
              2 * g * (int64_t)c.bn * c.bm <= a.part_floats;
     };
     const Cand cands[] = {
-        {&kRing[1], false, 0}, {&kRing[2], false, 0}, {&kRing[3], false, 0}, {&kRing[3], true, 0}};
-    const double rate_dp[] = {4.6, 4.05, 3.05}, rate_sk = 3.0, sk_fixed_us = 10.0;
+        {&kRing[0], false, 0}, {&kRing[1], false, 0}, {&kRing[2], false, 0}, {&kRing[2], true, 0}};
+    const double rate_dp[] = {4.8, 4.05, 3.05}, rate_sk = 3.0, sk_fixed_us = 10.0;
     const RingCfg* cfg = nullptr;
     bool sk = false;
     double best = 1e300;
