@@ -50,7 +50,9 @@ def parse():
                     help="7b-stage8-15-cold (default: one stage, cold TTFT) or one of "
                          "7b-full-b8, 13b-2x20-b4, 8b-4x8-ragged-merge (whole pipeline on "
                          "this GPU: batched prefill, decode, and for the last one KV "
-                         "export/import and merge)")
+                         "export/import and merge), 13b-4x10-scale-down (per-token decode "
+                         "times while the first stage loads the rest of the model in the "
+                         "background, then merges the others)")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="only run a few warm prefill steps and a 256 MiB device copy "
                          "(the workload for hardware-counter passes)")
@@ -121,6 +123,8 @@ def main():
     from paper_2502_15524_amd import hs, pipeline
     from workloads import WORKLOADS, gen
 
+    if args.workload.endswith("scale-down"):
+        return bench_scale_down(WORKLOADS[args.workload], args)
     if args.workload != "7b-stage8-15-cold":
         return bench_pipeline(WORKLOADS[args.workload], args)
     wl = WORKLOADS["7b-stage8-15-cold"]
@@ -580,6 +584,145 @@ def bench_pipeline(wl, args):
     res.update(res_extra)
     for st in stages:
         st.close()
+    print(json.dumps(res), flush=True)
+
+
+def bench_scale_down(wl, args):
+    """Scaling down: stage 0 serves layers [0, L/4) but reserves memory for
+    all L; after the batch's prefill it loads the remaining layers in the
+    background while the 4-stage pipeline keeps decoding, and once they have
+    landed it absorbs the other stages' KV cache (hs_stage_merge) and decodes
+    alone. Per-token (per-step) times are recorded, and a pipeline-only run
+    of the same length is the reference."""
+    import numpy as np
+    import torch
+    from paper_2502_15524_amd import hs, pipeline
+    from workloads import gen
+
+    cfg = wl.cfg
+    L = cfg.n_layers
+    lens = wl.lengths()
+    B, T, H, V = len(lens), sum(lens), cfg.hidden, cfg.vocab
+    n_dec = wl.decode_steps
+    max_ctx = max(lens) + n_dec + 16
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.Stream()
+    sp = stream.cuda_stream
+    c = pipeline.hs_cfg(cfg)
+
+    t0 = time.perf_counter()
+    full = pipeline.pinned_image(cfg, 0, L)
+    descs, nbytes = hs.hs_weight_layout(c, 0, L)
+    b0, e0 = wl.stages[0]
+    # stage 0's own part: the embedding and its layers (the final norm and the
+    # head, layer -1 like the embedding, sit at the end of the image)
+    first_end = max(d["offset"] + d["bytes"] for d in descs
+                    if 0 <= d["layer"] < e0 or d["kind"] == hs.HS_W_EMBED)
+    chunk = 64 << 20
+    s0 = pipeline.Stage(cfg, b0, e0, max_seqs=B + 2, max_ctx=max_ctx, max_batch_tokens=T,
+                        resident=(0, L))
+    for off in range(0, first_end, chunk):
+        hs.hs_stage_load_chunk(s0.h, off, full.data_ptr() + off, min(chunk, first_end - off))
+    s0.sync()
+    stages = [s0]
+    for b, e in wl.stages[1:]:
+        img = pipeline.pinned_image(cfg, b, e)
+        st = pipeline.Stage(cfg, b, e, max_seqs=B + 2, max_ctx=max_ctx, max_batch_tokens=T)
+        st.load(img, chunk)
+        st.sync()
+        img.close()
+        stages.append(st)
+    log(f"[bench] {wl.name}: stages {wl.stages}; stage 0 resident [0, {L}) with "
+        f"{first_end / 1e9:.2f} of {nbytes / 1e9:.2f} GB loaded; set-up "
+        f"{time.perf_counter() - t0:.1f} s")
+
+    toks = torch.from_numpy(gen.tokens(V, T, wl.seed)).to(dev)
+    hid = [torch.empty((T, H), dtype=torch.bfloat16, device=dev) for _ in range(2)]
+    hb = [torch.empty((B, H), dtype=torch.bfloat16, device=dev) for _ in range(2)]
+    nxt = torch.empty(B, dtype=torch.int32, device=dev)
+
+    def prefill(sts, ids):
+        x = toks
+        for i, st in enumerate(sts):
+            out = nxt if i == len(sts) - 1 else hid[i % 2]
+            st.prefill(ids, lens, x.data_ptr(), out.data_ptr(), 0, sp)
+            x = out
+        stream.synchronize()
+
+    def step(sts, ids):
+        x = nxt.clone()
+        t = time.perf_counter()
+        for i, st in enumerate(sts):
+            out = nxt if i == len(sts) - 1 else hb[i % 2]
+            st.decode(ids, x.data_ptr(), out.data_ptr(), 0, sp)
+            x = out
+        stream.synchronize()
+        return (time.perf_counter() - t) * 1e3
+
+    # reference: the pipeline decodes all tokens (no consolidation)
+    ids = list(range(100, 100 + B))
+    prefill(stages, ids)
+    ref = [step(stages, ids) for _ in range(n_dec)]
+    for st in stages:
+        for i in ids:
+            hs.hs_seq_free(st.h, i)
+    log(f"[bench] pipeline only: {np.mean(ref):.3f} ms/token-step "
+        f"({sum(ref):.1f} ms for {n_dec} steps)")
+
+    # scale-down run
+    ids = list(range(200, 200 + B))
+    prefill(stages, ids)
+    t_load0 = time.perf_counter()
+    for off in range(first_end, nbytes, chunk):
+        hs.hs_stage_load_chunk(s0.h, off, full.data_ptr() + off, min(chunk, nbytes - off))
+    times, merged_at, t_loaded, ms_merge = [], None, None, None
+    cur = stages
+    for k in range(n_dec):
+        times.append(step(cur, ids))
+        if merged_at is None:
+            _, wm = hs.hs_stage_loaded(s0.h)
+            if wm == nbytes:
+                t_loaded = (time.perf_counter() - t_load0) * 1e3
+                t = time.perf_counter()
+                hs.hs_stage_merge(s0.h, [st.h for st in stages[1:]], sp)
+                stream.synchronize()
+                ms_merge = (time.perf_counter() - t) * 1e3
+                merged_at = k + 1
+                cur = [s0]
+    assert merged_at is not None, "background load did not finish within the decode steps"
+    during = times[:merged_at]
+    after = times[merged_at:]
+    total_sd = sum(times) + ms_merge
+    log(f"[bench] scale-down: background load of {(nbytes - first_end) / 1e9:.2f} GB landed "
+        f"after {t_loaded:.1f} ms ({(nbytes - first_end) / (t_loaded / 1e3) / 1e9:.1f} GB/s); "
+        f"{merged_at} steps during the load at {np.mean(during):.3f} ms/step "
+        f"(pipeline only {np.mean(ref):.3f}); merge {ms_merge:.2f} ms; "
+        f"{len(after)} steps after at {np.mean(after) if after else float('nan'):.3f} ms/step; "
+        f"generation {total_sd:.1f} ms vs {sum(ref):.1f} ms pipeline only")
+    res = {
+        "metric": METRIC, "value": round(B * n_dec / (total_sd / 1e3), 1), "unit": "tok/s",
+        "n_gpus": 1, "steps": n_dec, "warmup": 0, "ms_per_step": round(total_sd / n_dec, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "model_shape": cfg.name, "stages": wl.stages,
+                   "batch": B, "prompt_len": lens[0], "generated_tokens": n_dec},
+        "roofline": None, "cpu_baseline": None,
+        "background_load_bytes": nbytes - first_end,
+        "background_load_ms": round(t_loaded, 2),
+        "background_load_GBps": round((nbytes - first_end) / (t_loaded / 1e3) / 1e9, 2),
+        "steps_during_load": merged_at,
+        "ms_per_step_during_load": round(float(np.mean(during)), 4),
+        "ms_per_step_pipeline_only": round(float(np.mean(ref)), 4),
+        "merge_ms": round(ms_merge, 3),
+        "ms_per_step_after_merge": round(float(np.mean(after)), 4) if after else None,
+        "generation_ms_scale_down": round(total_sd, 2),
+        "generation_ms_pipeline_only": round(sum(ref), 2),
+        "per_step_ms_scale_down": [round(t, 3) for t in times],
+        "per_step_ms_pipeline_only": [round(t, 3) for t in ref],
+    }
+    for st in stages:
+        st.close()
+    full.close()
     print(json.dumps(res), flush=True)
 
 

@@ -376,3 +376,63 @@ def _hidden_prefill_full(st, tokens, seq_id):
     st.prefill([seq_id], [len(tokens)], x.data_ptr(), nxt.data_ptr(), logits.data_ptr(),
                G.stream_ptr())
     return logits.cpu().numpy()
+
+
+def test_scale_down_background_load_then_merge(env):
+    """Scaling down: stage 0 serves layer 0 with memory for both layers and
+    only layer 0's bytes loaded; it loads layer 1 (and the head) while the
+    two-stage pipeline keeps decoding, then absorbs stage 1's KV cache and
+    decodes alone. Tokens and logits equal an uninterrupted pipeline's,
+    bitwise."""
+    hs = env["hs"]
+    torch = G.torch()
+    sp = G.stream_ptr()
+    ref_toks, ref_lgs = run_greedy([make(env, 0, 1), make(env, 1, 2)], env["prompt"], 9,
+                                   seq_id=4)
+    c = env["pipeline"].hs_cfg(CFG)
+    descs, nbytes = hs.hs_weight_layout(c, 0, 2)
+    first_end = max(d["offset"] + d["bytes"] for d in descs
+                    if 0 <= d["layer"] < 1 or d["kind"] == hs.HS_W_EMBED)
+    assert 0 < first_end < nbytes
+    img = env["imgs"][(0, 2)]
+    s0 = make(env, 0, 1, resident=(0, 2), load=False)
+    hs.hs_stage_load_chunk(s0.h, 0, img.data_ptr(), first_end)
+    s1 = make(env, 1, 2)
+    assert hs.hs_stage_loaded(s0.h)[0] >= 1
+
+    T = len(env["prompt"])
+    x = torch.from_numpy(np.asarray(env["prompt"], np.int32)).cuda()
+    hid = torch.zeros((T, CFG.hidden), dtype=torch.bfloat16, device="cuda")
+    nxt = torch.zeros(1, dtype=torch.int32, device="cuda")
+    lg = torch.zeros((1, CFG.vocab), dtype=torch.float32, device="cuda")
+    s0.prefill([4], [T], x.data_ptr(), hid.data_ptr(), 0, sp)
+    s1.prefill([4], [T], hid.data_ptr(), nxt.data_ptr(), lg.data_ptr(), sp)
+    toks, lgs = [int(nxt.item())], [lg.cpu().numpy()[0].copy()]
+
+    def decode(stages):
+        xi = nxt.clone()
+        for st in stages:
+            if st.end == CFG.n_layers:
+                st.decode([4], xi.data_ptr(), nxt.data_ptr(), lg.data_ptr(), sp)
+            else:
+                out = torch.zeros((1, CFG.hidden), dtype=torch.bfloat16, device="cuda")
+                st.decode([4], xi.data_ptr(), out.data_ptr(), 0, sp)
+                xi = out
+        toks.append(int(nxt.item()))
+        lgs.append(lg.cpu().numpy()[0].copy())
+
+    for _ in range(3):
+        decode([s0, s1])
+    step = 4096
+    for off in range(first_end, nbytes, step):       # background load, small chunks
+        hs.hs_stage_load_chunk(s0.h, off, img.data_ptr() + off, min(step, nbytes - off))
+    for _ in range(3):
+        decode([s0, s1])                              # while the chunks land
+    s0.sync()
+    assert hs.hs_stage_loaded(s0.h) == (2, nbytes)
+    hs.hs_stage_merge(s0.h, [s1.h], sp)
+    assert (s0.begin, s0.end) == (0, 2) and s1.info()["live_seqs"] == 0
+    for _ in range(3):
+        decode([s0])
+    assert np.array_equal(np.array(toks, np.int32), ref_toks)
+    assert np.array_equal(np.stack(lgs), ref_lgs)

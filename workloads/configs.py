@@ -118,6 +118,14 @@ WORKLOADS = {
                                     _even(32, 4), batch=16, prompt_lens=None,
                                     decode_steps=256, seed=5,
                                     ragged=(128, 2048, 16, 0)),
+    # Scaling down (the consolidation study of the evaluation): 13B shape in
+    # 4 stages of 10 layers, 512-token prompts, 512 generated tokens. The
+    # first stage holds all 40 layers' memory, loads the rest of the model in
+    # the background while the pipeline decodes, then absorbs the others'
+    # KV cache and decodes alone.
+    "13b-4x10-scale-down": Workload("13b-4x10-scale-down", "llama2-13b", _even(40, 4),
+                                    batch=4, prompt_lens=(512,) * 4, decode_steps=512,
+                                    seed=6),
 }
 
 
