@@ -305,6 +305,37 @@ hs_status hs_kv_export(hs_stage* st, int32_t n_seqs, const int64_t* seq_ids,
 hs_status hs_kv_import(hs_stage* st, const void* src, uint64_t bytes,
                        void* stream);
 
+/* Host-staged (streaming) migration, the form that crosses machines
+ * (section 6.2: blocks leave the GPU in chunks that are sent on as soon as
+ * they reach host memory, and on the receiving worker each arriving chunk
+ * is loaded to the GPU on its own stream). Blobs are the same bytes as
+ * above; chunks are whole KV units of about `chunk_bytes` (the first one
+ * also carries the header and records).
+ *
+ * hs_kv_export_host: like hs_kv_export, but `dst` is pinned host memory
+ * (hipHostMalloc). The blocks are gathered chunk by chunk into a device
+ * staging buffer owned by the stage (grown on demand) and every chunk is
+ * copied to `dst` on the stage's copy streams as soon as it is gathered.
+ * hs_kv_host_progress reports the landed prefix without blocking; the call
+ * as a whole is complete (ordered on `stream` and for later calls) when
+ * every chunk has landed.
+ *
+ * hs_kv_import_host: like hs_kv_import, but `src` is a complete blob in
+ * pinned host memory. The header is read from host memory; the chunks are
+ * copied to the staging buffer on the copy streams and each chunk's units
+ * are scattered into the pools (on `stream`) as soon as it has landed.
+ *
+ * Errors: as hs_kv_export / hs_kv_import; HS_EINVAL also for memory that is
+ * not pinned host memory or chunk_bytes == 0; HS_ENOMEM when the staging
+ * buffer cannot grow. */
+hs_status hs_kv_export_host(hs_stage* st, int32_t n_seqs, const int64_t* seq_ids,
+                            void* dst, uint64_t cap, uint64_t chunk_bytes,
+                            uint64_t* written, void* stream);
+hs_status hs_kv_import_host(hs_stage* st, const void* src, uint64_t bytes,
+                            uint64_t chunk_bytes, void* stream);
+/* Bytes of the last host-staged transfer that have landed, as a prefix. */
+hs_status hs_kv_host_progress(hs_stage* st, uint64_t* landed);
+
 /* Consolidate: `dst` takes over the sequences of the `n_srcs` source stages
  * (section 6.1 scaling down). The serving ranges of dst (if not empty) and
  * of all sources must be disjoint and together contiguous, within dst's

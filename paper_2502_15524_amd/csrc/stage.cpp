@@ -126,6 +126,17 @@ struct hs_stage {
   hipEvent_t desc_ev = nullptr;
   bool desc_used = false;
 
+  // host-staged KV migration: device staging blob and the chunk copies of
+  // the last transfer (offset, bytes, completion event)
+  uint8_t* d_stage = nullptr;
+  uint64_t stage_cap = 0;
+  struct Xfer {
+    uint64_t off, bytes;
+    hipEvent_t ev;
+    bool done;
+  };
+  std::vector<Xfer> xfer;
+
   bool timing = false;
   std::string timing_sites;  // ",site,site," or empty for every site
   std::vector<Pending> pending;
@@ -157,6 +168,8 @@ hs_stage::~hs_stage() {
   if (last_done) (void)hipEventDestroy(last_done);
   if (compute) (void)hipStreamDestroy(compute);
   for (auto s : copy) (void)hipStreamDestroy(s);
+  for (auto& x : xfer) (void)hipEventDestroy(x.ev);
+  if (d_stage) (void)hipFree(d_stage);
   if (d_ws) (void)hipFree(d_ws);
   if (d_cos) (void)hipFree(d_cos);
   if (d_sin) (void)hipFree(d_sin);
@@ -467,6 +480,16 @@ bool is_device_ptr(const void* p) {
   return a.type == hipMemoryTypeDevice;
 }
 
+bool is_pinned_host_ptr(const void* p) {
+  if (!p) return false;
+  hipPointerAttribute_t a;
+  if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return a.type == hipMemoryTypeHost;
+}
+
 // Grow the KV-copy descriptor buffers to hold n units.
 hs_status desc_reserve(hs_stage* st, uint64_t n) {
   const uint64_t need = al(n * 8) * 2 + al(n * 4);
@@ -522,6 +545,125 @@ hs_status copy_units(hs_stage* st, const Units& u, int zero_tail, hipStream_t s,
   HIPTRY(hipEventRecord(st->desc_ev, s));
   st->desc_used = true;
   return HS_OK;
+}
+
+// Upload the descriptors of `u` (and a blob header to head_dst) on stream s
+// without launching; returns the device views.
+hs_status desc_upload(hs_stage* st, const Units& u, hipStream_t s, const std::vector<uint8_t>* head,
+                      void* head_dst, const uint64_t** dsrc, const uint64_t** ddst,
+                      const int32_t** dval) {
+  const uint64_t n = u.src.size();
+  const uint64_t hb = head ? al(head->size()) : 0;
+  hs_status r = desc_reserve(st, n + hb / 8 + 1);
+  if (r != HS_OK) return r;
+  uint8_t* h = st->h_desc;
+  const uint64_t o_dst = al(n * 8), o_val = 2 * al(n * 8), o_head = o_val + al(n * 4);
+  memcpy(h, u.src.data(), n * 8);
+  memcpy(h + o_dst, u.dst.data(), n * 8);
+  memcpy(h + o_val, u.valid.data(), n * 4);
+  if (head) memcpy(h + o_head, head->data(), head->size());
+  HIPTRY(hipMemcpyAsync(st->d_desc, h, o_head + hb, hipMemcpyHostToDevice, s));
+  if (head) HIPTRY(hipMemcpyAsync(head_dst, st->d_desc + o_head, head->size(),
+                                  hipMemcpyDeviceToDevice, s));
+  *dsrc = reinterpret_cast<const uint64_t*>(st->d_desc);
+  *ddst = reinterpret_cast<const uint64_t*>(st->d_desc + o_dst);
+  *dval = reinterpret_cast<const int32_t*>(st->d_desc + o_val);
+  return HS_OK;
+}
+
+// Grow the device staging blob of host-staged migration. Growing waits for
+// the stage's queued work (the old buffer may still be in use).
+hs_status stage_buffer(hs_stage* st, uint64_t bytes) {
+  if (bytes <= st->stage_cap) return HS_OK;
+  if (st->last_valid) HIPTRY(hipEventSynchronize(st->last_done));
+  for (auto c : st->copy) HIPTRY(hipStreamSynchronize(c));
+  if (st->d_stage) HIPTRY(hipFree(st->d_stage));
+  st->d_stage = nullptr;
+  st->stage_cap = 0;
+  if (hipMalloc(reinterpret_cast<void**>(&st->d_stage), bytes) != hipSuccess)
+    return fail(HS_ENOMEM, "KV staging buffer allocation failed");
+  st->stage_cap = bytes;
+  return HS_OK;
+}
+
+// Forget the previous transfer's chunk events (the stage's ordering already
+// covers them: every transfer joins its copy streams into the call stream).
+void xfer_reset(hs_stage* st) {
+  for (auto& x : st->xfer) (void)hipEventDestroy(x.ev);
+  st->xfer.clear();
+}
+
+// Validate a blob header held in host memory against the stage and reserve
+// its sequences (new sequences get fresh blocks). On error nothing changes.
+hs_status import_reserve(hs_stage* st, const uint8_t* head, uint64_t head_len, uint64_t bytes,
+                         BlobHeader* hout, std::vector<BlobRecord>* rout) {
+  BlobHeader h;
+  std::vector<BlobRecord> recs;
+  hs_status r = blob_decode_head(head, head_len, &h, &recs);
+  if (r != HS_OK) return r;
+  if (h.total_bytes != bytes) return fail(HS_EINVAL, "blob length does not match its header");
+  if (h.n_kv_heads != st->cfg.n_kv_heads || h.head_dim != st->cfg.head_dim ||
+      h.block_size != kBlock)
+    return fail(HS_EINVAL, "blob KV geometry differs from the stage's");
+  if (h.layer_begin < st->rb || h.layer_end > st->re)
+    return fail(HS_EINVAL, "blob layers are not resident in this stage");
+  int64_t need_blocks = 0, new_seqs = 0;
+  for (const BlobRecord& rc : recs) {
+    if (rc.n_tokens > st->opts.max_ctx) return fail(HS_EINVAL, "blob sequence longer than max_ctx");
+    auto it = st->seqs.find(rc.seq_id);
+    if (it == st->seqs.end()) {
+      need_blocks += rc.n_blocks;
+      ++new_seqs;
+    } else {
+      const Seq& q = it->second;
+      if (q.n_tokens != rc.n_tokens)
+        return fail(HS_EINVAL, "blob token count differs from the live sequence's");
+      if (!(h.layer_end == q.kv_begin || h.layer_begin == q.kv_end ||
+            (h.layer_begin >= q.kv_begin && h.layer_end <= q.kv_end)))
+        return fail(HS_EINVAL, "blob layers are not adjacent to the sequence's cached layers");
+    }
+  }
+  if ((int64_t)st->seqs.size() + new_seqs > st->opts.max_seqs)
+    return fail(HS_ENOMEM, "no free sequence slots");
+  if (need_blocks > (int64_t)st->free_blocks.size()) return fail(HS_ENOMEM, "not enough free KV blocks");
+  for (const BlobRecord& rc : recs) {
+    auto it = st->seqs.find(rc.seq_id);
+    if (it == st->seqs.end()) {
+      Seq q;
+      q.n_tokens = rc.n_tokens;
+      q.kv_begin = h.layer_begin;
+      q.kv_end = h.layer_end;
+      for (int b = 0; b < rc.n_blocks; ++b) {
+        q.blocks.push_back(st->free_blocks.back());
+        st->free_blocks.pop_back();
+      }
+      st->seqs.emplace(rc.seq_id, std::move(q));
+    } else {
+      Seq& q = it->second;
+      q.kv_begin = std::min(q.kv_begin, h.layer_begin);
+      q.kv_end = std::max(q.kv_end, h.layer_end);
+    }
+  }
+  *hout = h;
+  *rout = std::move(recs);
+  return HS_OK;
+}
+
+// Units of an import: blob payload (at base) -> the stage's pools.
+Units import_units(hs_stage* st, const BlobHeader& h, const std::vector<BlobRecord>& recs,
+                   uint64_t base) {
+  Units u;
+  uint64_t unit = 0;
+  for (int l = h.layer_begin; l < h.layer_end; ++l)
+    for (const BlobRecord& rc : recs) {
+      const Seq& q = st->seqs.at(rc.seq_id);
+      for (int b = 0; b < rc.n_blocks; ++b, ++unit) {
+        u.src.push_back(base + h.payload_offset + unit * st->unit_bytes);
+        u.dst.push_back((uint64_t)(uintptr_t)pool(st, l) + (uint64_t)q.blocks[b] * st->unit_bytes);
+        u.valid.push_back(kBlock);
+      }
+    }
+  return u;
 }
 
 bool same_model(const hs_model_cfg& a, const hs_model_cfg& b) {
@@ -1151,66 +1293,185 @@ extern "C" hs_status hs_kv_import(hs_stage* st, const void* src, uint64_t bytes,
   }
   BlobHeader h;
   std::vector<BlobRecord> recs;
-  r = blob_decode_head(head.data(), head.size(), &h, &recs);
+  r = import_reserve(st, head.data(), head.size(), bytes, &h, &recs);
   if (r != HS_OK) return r;
-  if (h.total_bytes != bytes) return fail(HS_EINVAL, "blob length does not match its header");
-  if (h.n_kv_heads != st->cfg.n_kv_heads || h.head_dim != st->cfg.head_dim ||
-      h.block_size != kBlock)
-    return fail(HS_EINVAL, "blob KV geometry differs from the stage's");
-  if (h.layer_begin < st->rb || h.layer_end > st->re)
-    return fail(HS_EINVAL, "blob layers are not resident in this stage");
-  int64_t need_blocks = 0, new_seqs = 0;
-  for (const BlobRecord& rc : recs) {
-    if (rc.n_tokens > st->opts.max_ctx) return fail(HS_EINVAL, "blob sequence longer than max_ctx");
-    auto it = st->seqs.find(rc.seq_id);
-    if (it == st->seqs.end()) {
-      need_blocks += rc.n_blocks;
-      ++new_seqs;
-    } else {
-      const Seq& q = it->second;
-      if (q.n_tokens != rc.n_tokens)
-        return fail(HS_EINVAL, "blob token count differs from the live sequence's");
-      if (!(h.layer_end == q.kv_begin || h.layer_begin == q.kv_end ||
-            (h.layer_begin >= q.kv_begin && h.layer_end <= q.kv_end)))
-        return fail(HS_EINVAL, "blob layers are not adjacent to the sequence's cached layers");
-    }
-  }
-  if ((int64_t)st->seqs.size() + new_seqs > st->opts.max_seqs)
-    return fail(HS_ENOMEM, "no free sequence slots");
-  if (need_blocks > (int64_t)st->free_blocks.size()) return fail(HS_ENOMEM, "not enough free KV blocks");
-
-  for (const BlobRecord& rc : recs) {
-    auto it = st->seqs.find(rc.seq_id);
-    if (it == st->seqs.end()) {
-      Seq q;
-      q.n_tokens = rc.n_tokens;
-      q.kv_begin = h.layer_begin;
-      q.kv_end = h.layer_end;
-      for (int b = 0; b < rc.n_blocks; ++b) {
-        q.blocks.push_back(st->free_blocks.back());
-        st->free_blocks.pop_back();
-      }
-      st->seqs.emplace(rc.seq_id, std::move(q));
-    } else {
-      Seq& q = it->second;
-      q.kv_begin = std::min(q.kv_begin, h.layer_begin);
-      q.kv_end = std::max(q.kv_end, h.layer_end);
-    }
-  }
-  Units u;
-  uint64_t unit = 0;
-  for (int l = h.layer_begin; l < h.layer_end; ++l)
-    for (const BlobRecord& rc : recs) {
-      const Seq& q = st->seqs.at(rc.seq_id);
-      for (int b = 0; b < rc.n_blocks; ++b, ++unit) {
-        u.src.push_back((uint64_t)(uintptr_t)src + h.payload_offset + unit * st->unit_bytes);
-        u.dst.push_back((uint64_t)(uintptr_t)pool(st, l) + (uint64_t)q.blocks[b] * st->unit_bytes);
-        u.valid.push_back(kBlock);
-      }
-    }
+  Units u = import_units(st, h, recs, (uint64_t)(uintptr_t)src);
   r = copy_units(st, u, 0, s);
   if (r != HS_OK) return r;
   return end_call(st, s);
+  ABI_END
+}
+
+// Host-staged migration: chunks are whole KV units; chunk j covers units
+// [j * cu, (j + 1) * cu) (plus the header and records in the first chunk).
+namespace {
+struct ChunkPlan {
+  uint64_t cu;        // units per chunk
+  uint64_t n_chunks;
+  uint64_t first, count;  // of chunk j, filled by at()
+  uint64_t off, bytes;
+};
+ChunkPlan plan_chunks(const hs_stage* st, const BlobHeader& h, uint64_t units, uint64_t chunk_bytes) {
+  ChunkPlan p{};
+  p.cu = std::max<uint64_t>(1, chunk_bytes / st->unit_bytes);
+  p.n_chunks = std::max<uint64_t>(1, (units + p.cu - 1) / p.cu);
+  (void)h;
+  return p;
+}
+void chunk_at(const hs_stage* st, const BlobHeader& h, uint64_t units, ChunkPlan* p, uint64_t j) {
+  p->first = j * p->cu;
+  p->count = std::min(p->cu, units - std::min(units, p->first));
+  const uint64_t b0 = j == 0 ? 0 : h.payload_offset + p->first * st->unit_bytes;
+  const uint64_t b1 = j + 1 == p->n_chunks ? h.total_bytes
+                                           : h.payload_offset + (p->first + p->count) * st->unit_bytes;
+  p->off = b0;
+  p->bytes = b1 - b0;
+}
+}  // namespace
+
+extern "C" hs_status hs_kv_export_host(hs_stage* st, int32_t n, const int64_t* ids, void* dst,
+                                       uint64_t cap, uint64_t chunk_bytes, uint64_t* written,
+                                       void* stream) {
+  ABI_BEGIN
+  if (!st || !written || !dst) return fail(HS_EINVAL, "null argument");
+  if (chunk_bytes == 0) return fail(HS_EINVAL, "chunk_bytes must be positive");
+  std::vector<BlobRecord> recs;
+  BlobHeader h;
+  hs_status r = export_records(st, n, ids, &recs, &h);
+  if (r != HS_OK) return r;
+  *written = h.total_bytes;
+  if (cap < h.total_bytes) return fail(HS_ERANGE, "destination smaller than the blob");
+  DeviceGuard dg(st->device);
+  if (!is_pinned_host_ptr(dst)) return fail(HS_EINVAL, "blob destination must be pinned host memory");
+  r = stage_buffer(st, h.total_bytes);
+  if (r != HS_OK) return r;
+  std::vector<uint8_t> head = blob_encode_head(h, recs);
+  Units u;
+  uint64_t unit = 0;
+  for (int l = st->begin; l < st->end; ++l)
+    for (const BlobRecord& rc : recs) {
+      const Seq& q = st->seqs.at(rc.seq_id);
+      for (int b = 0; b < rc.n_blocks; ++b, ++unit) {
+        u.src.push_back((uint64_t)(uintptr_t)pool(st, l) + (uint64_t)q.blocks[b] * st->unit_bytes);
+        u.dst.push_back((uint64_t)(uintptr_t)st->d_stage + h.payload_offset + unit * st->unit_bytes);
+        u.valid.push_back(std::min(kBlock, rc.n_tokens - b * kBlock));
+      }
+    }
+  hipStream_t s = pick(st, stream);
+  r = begin_call(st, s);
+  if (r != HS_OK) return r;
+  xfer_reset(st);
+  const uint64_t* dsrc;
+  const uint64_t* ddst;
+  const int32_t* dval;
+  r = desc_upload(st, u, s, &head, st->d_stage, &dsrc, &ddst, &dval);
+  if (r != HS_OK) return r;
+  ChunkPlan p = plan_chunks(st, h, unit, chunk_bytes);
+  std::vector<bool> used(st->copy.size(), false);
+  for (uint64_t j = 0; j < p.n_chunks; ++j) {
+    chunk_at(st, h, unit, &p, j);
+    if (p.count > 0) {
+      r = run(st, s, "kv_copy", [&](LaunchInfo* i) {
+        return kv_copy(dsrc + p.first, ddst + p.first, dval + p.first, (int)p.count,
+                       (int64_t)st->unit_bytes, st->cfg.head_dim, 1, s, i);
+      });
+      if (r != HS_OK) return r;
+    }
+    hipEvent_t gathered = nullptr, landed = nullptr;
+    HIPTRY(hipEventCreateWithFlags(&gathered, hipEventDisableTiming));
+    HIPTRY(hipEventCreateWithFlags(&landed, hipEventDisableTiming));
+    st->xfer.push_back({p.off, p.bytes, landed, false});
+    HIPTRY(hipEventRecord(gathered, s));
+    const int ci = (int)(j % st->copy.size());
+    hipStream_t cs = st->copy[ci];
+    used[ci] = true;
+    HIPTRY(hipStreamWaitEvent(cs, gathered, 0));
+    HIPTRY(hipMemcpyAsync(static_cast<uint8_t*>(dst) + p.off, st->d_stage + p.off, p.bytes,
+                          hipMemcpyDeviceToHost, cs));
+    HIPTRY(hipEventRecord(landed, cs));
+    HIPTRY(hipEventDestroy(gathered));  // released once recorded work completes
+  }
+  HIPTRY(hipEventRecord(st->desc_ev, s));
+  st->desc_used = true;
+  // the call completes when every chunk has landed
+  for (const auto& x : st->xfer) HIPTRY(hipStreamWaitEvent(s, x.ev, 0));
+  return end_call(st, s);
+  ABI_END
+}
+
+extern "C" hs_status hs_kv_import_host(hs_stage* st, const void* src, uint64_t bytes,
+                                       uint64_t chunk_bytes, void* stream) {
+  ABI_BEGIN
+  if (!st || !src) return fail(HS_EINVAL, "null argument");
+  if (chunk_bytes == 0) return fail(HS_EINVAL, "chunk_bytes must be positive");
+  if (bytes < kBlobHeader) return fail(HS_EINVAL, "blob shorter than its header");
+  DeviceGuard dg(st->device);
+  if (!is_pinned_host_ptr(src)) return fail(HS_EINVAL, "blob source must be pinned host memory");
+  const uint8_t* hb = static_cast<const uint8_t*>(src);
+  int32_t ns = 0;
+  memcpy(&ns, hb + 32, 4);
+  if (ns < 0 || kBlobHeader + kBlobRecord * (uint64_t)ns > bytes)
+    return fail(HS_EINVAL, "blob sequence count does not fit its length");
+  hipStream_t s = pick(st, stream);
+  // the staging buffer must be free before the reservation changes state
+  hs_status r = stage_buffer(st, bytes);
+  if (r != HS_OK) return r;
+  BlobHeader h;
+  std::vector<BlobRecord> recs;
+  r = import_reserve(st, hb, kBlobHeader + kBlobRecord * (uint64_t)ns, bytes, &h, &recs);
+  if (r != HS_OK) return r;
+  Units u = import_units(st, h, recs, (uint64_t)(uintptr_t)st->d_stage);
+  r = begin_call(st, s);
+  if (r != HS_OK) return r;
+  xfer_reset(st);
+  const uint64_t* dsrc;
+  const uint64_t* ddst;
+  const int32_t* dval;
+  r = desc_upload(st, u, s, nullptr, nullptr, &dsrc, &ddst, &dval);
+  if (r != HS_OK) return r;
+  hipEvent_t ready = nullptr;  // earlier work on the staging buffer is done
+  HIPTRY(hipEventCreateWithFlags(&ready, hipEventDisableTiming));
+  HIPTRY(hipEventRecord(ready, s));
+  for (auto c : st->copy) HIPTRY(hipStreamWaitEvent(c, ready, 0));
+  HIPTRY(hipEventDestroy(ready));
+  const uint64_t units = u.src.size();
+  ChunkPlan p = plan_chunks(st, h, units, chunk_bytes);
+  for (uint64_t j = 0; j < p.n_chunks; ++j) {
+    chunk_at(st, h, units, &p, j);
+    hipStream_t cs = st->copy[j % st->copy.size()];
+    hipEvent_t landed = nullptr;
+    HIPTRY(hipEventCreateWithFlags(&landed, hipEventDisableTiming));
+    st->xfer.push_back({p.off, p.bytes, landed, false});
+    HIPTRY(hipMemcpyAsync(st->d_stage + p.off, hb + p.off, p.bytes, hipMemcpyHostToDevice, cs));
+    HIPTRY(hipEventRecord(landed, cs));
+    // scatter this chunk's units as soon as it has landed
+    HIPTRY(hipStreamWaitEvent(s, landed, 0));
+    if (p.count > 0) {
+      r = run(st, s, "kv_copy", [&](LaunchInfo* i) {
+        return kv_copy(dsrc + p.first, ddst + p.first, dval + p.first, (int)p.count,
+                       (int64_t)st->unit_bytes, st->cfg.head_dim, 0, s, i);
+      });
+      if (r != HS_OK) return r;
+    }
+  }
+  HIPTRY(hipEventRecord(st->desc_ev, s));
+  st->desc_used = true;
+  return end_call(st, s);
+  ABI_END
+}
+
+extern "C" hs_status hs_kv_host_progress(hs_stage* st, uint64_t* landed) {
+  ABI_BEGIN
+  if (!st || !landed) return fail(HS_EINVAL, "null argument");
+  DeviceGuard dg(st->device);
+  uint64_t pos = 0;
+  for (auto& x : st->xfer) {
+    if (!x.done && hipEventQuery(x.ev) == hipSuccess) x.done = true;
+    if (x.off != pos || !x.done) break;
+    pos = x.off + x.bytes;
+  }
+  *landed = pos;
+  return HS_OK;
   ABI_END
 }
 

@@ -97,6 +97,10 @@ _SIGS = {
     "hs_kv_export": [_P, C.c_int32, C.POINTER(C.c_int64), _P, C.c_uint64,
                      C.POINTER(C.c_uint64), _P],
     "hs_kv_import": [_P, _P, C.c_uint64, _P],
+    "hs_kv_export_host": [_P, C.c_int32, C.POINTER(C.c_int64), _P, C.c_uint64, C.c_uint64,
+                          C.POINTER(C.c_uint64), _P],
+    "hs_kv_import_host": [_P, _P, C.c_uint64, C.c_uint64, _P],
+    "hs_kv_host_progress": [_P, C.POINTER(C.c_uint64)],
     "hs_stage_merge": [_P, C.POINTER(_P), C.c_int32, _P],
     "hs_kv_blob_describe": [_P, C.c_uint64, C.POINTER(hs_kv_blob_info)],
     "hs_stage_set_timing": [_P, C.c_int32],
@@ -277,6 +281,30 @@ def hs_kv_export(h, seq_ids, dst_ptr, cap, stream=0):
 
 def hs_kv_import(h, src_ptr, nbytes, stream=0):
     _check(lib().hs_kv_import(h, src_ptr, nbytes, stream or None))
+
+
+def hs_kv_export_host(h, seq_ids, host_dst, cap, chunk_bytes=64 << 20, stream=0):
+    """Export into pinned host memory in chunks; returns the blob size."""
+    ids, n = _i64(seq_ids)
+    w = C.c_uint64(0)
+    code = lib().hs_kv_export_host(h, n, ids, host_dst, cap, chunk_bytes, C.byref(w),
+                                   stream or None)
+    if code == HS_ERANGE:
+        err = HSError(code, hs_last_error())
+        err.required = w.value
+        raise err
+    _check(code)
+    return w.value
+
+
+def hs_kv_import_host(h, host_src, nbytes, chunk_bytes=64 << 20, stream=0):
+    _check(lib().hs_kv_import_host(h, host_src, nbytes, chunk_bytes, stream or None))
+
+
+def hs_kv_host_progress(h):
+    v = C.c_uint64(0)
+    _check(lib().hs_kv_host_progress(h, C.byref(v)))
+    return v.value
 
 
 def hs_stage_merge(dst, srcs, stream=0):

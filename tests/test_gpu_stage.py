@@ -436,3 +436,49 @@ def test_scale_down_background_load_then_merge(env):
         decode([s0])
     assert np.array_equal(np.array(toks, np.int32), ref_toks)
     assert np.array_equal(np.stack(lgs), ref_lgs)
+
+
+def test_host_staged_migration_bitwise(env):
+    """Host-staged migration: the blob written to pinned host memory chunk by
+    chunk equals the device export byte for byte, its progress reaches the
+    whole blob, and a stage that imports it from host memory (chunked) decodes
+    exactly like the original."""
+    torch = G.torch()
+    hs = env["hs"]
+    sp = G.stream_ptr()
+    full = make(env, 0, 2)
+    t_ref, _ = run_greedy([full], env["prompt"], 0, seq_id=8)
+    dev_blob = _export(full, [8]).cpu().numpy().tobytes()
+    size = len(dev_blob)
+    host = torch.zeros(size + 64, dtype=torch.uint8).pin_memory()
+    unit = 2 * 2 * CFG.n_kv_heads * 16 * CFG.head_dim      # one KV unit: K and V blocks
+    for chunk in (unit, 3 * unit + 5, 1 << 30):
+        host.zero_()
+        n = hs.hs_kv_export_host(full.h, [8], host.data_ptr(), size + 64, chunk, sp)
+        assert n == size
+        full.sync()
+        assert hs.hs_kv_host_progress(full.h) == size
+        assert host[:size].numpy().tobytes() == dev_blob
+    fresh = make(env, 0, 2)
+    hs.hs_kv_import_host(fresh.h, host.data_ptr(), size, 2 * unit, sp)
+    assert hs.hs_seq_tokens(fresh.h, 8) == len(env["prompt"])
+    assert _export(fresh, [8]).cpu().numpy().tobytes() == dev_blob
+    outs = []
+    for st in (full, fresh):
+        nxt = torch.tensor([int(t_ref[0])], dtype=torch.int32, device="cuda")
+        lg = torch.zeros((1, CFG.vocab), dtype=torch.float32, device="cuda")
+        seq = []
+        for _ in range(4):
+            inp = nxt.clone()
+            st.decode([8], inp.data_ptr(), nxt.data_ptr(), lg.data_ptr(), sp)
+            seq.append(lg.cpu().numpy().copy())
+        outs.append(np.stack(seq))
+    assert np.array_equal(outs[0], outs[1])
+    size2 = hs.hs_kv_export_size(full.h, [8])     # the sequence grew while decoding
+    dev = torch.zeros(size2, dtype=torch.uint8, device="cuda")
+    with pytest.raises(hs.HSError) as e:       # device memory is not a host blob
+        hs.hs_kv_export_host(full.h, [8], dev.data_ptr(), size2, unit, sp)
+    assert e.value.code == hs.HS_EINVAL
+    with pytest.raises(hs.HSError) as e:
+        hs.hs_kv_export_host(full.h, [8], host.data_ptr(), size2 - 1, unit, sp)
+    assert e.value.code == hs.HS_ERANGE and e.value.required == size2
