@@ -482,3 +482,75 @@ def test_host_staged_migration_bitwise(env):
     with pytest.raises(hs.HSError) as e:
         hs.hs_kv_export_host(full.h, [8], host.data_ptr(), size2 - 1, unit, sp)
     assert e.value.code == hs.HS_ERANGE and e.value.required == size2
+
+
+def test_continuous_batching_then_merge_bitwise(env):
+    """Sequences join (prefilled one per call) and leave between decode steps
+    of a two-stage pipeline whose first stage can hold both layers; midway the
+    pipeline is drained and merged into that stage. Every sequence's logits at
+    every step equal those of the sequence decoded alone, bitwise (decode
+    arithmetic is per row, so batch composition does not change the bits)."""
+    hs = env["hs"]
+    torch = G.torch()
+    sp = G.stream_ptr()
+    prompts = {11: env["prompt"], 12: gen.tokens(CFG.vocab, 40, 21),
+               13: gen.tokens(CFG.vocab, 17, 22)}
+
+    def alone(sid, n):
+        toks, lgs = run_greedy([make(env, 0, 1), make(env, 1, 2)], prompts[sid], n, seq_id=sid)
+        return lgs
+
+    ref = {11: alone(11, 5), 12: alone(12, 6), 13: alone(13, 3)}
+    s0 = make(env, 0, 1, resident=(0, 2))
+    s1 = make(env, 1, 2)
+    got = {sid: [] for sid in prompts}
+    nxt = {}
+
+    def prefill(stages, sid):
+        p = prompts[sid]
+        T = len(p)
+        x = torch.from_numpy(np.asarray(p, np.int32)).cuda()
+        hid = torch.zeros((T, CFG.hidden), dtype=torch.bfloat16, device="cuda")
+        tok = torch.zeros(1, dtype=torch.int32, device="cuda")
+        lg = torch.zeros((1, CFG.vocab), dtype=torch.float32, device="cuda")
+        stages[0].prefill([sid], [T], x.data_ptr(), hid.data_ptr(), 0, sp)
+        stages[1].prefill([sid], [T], hid.data_ptr(), tok.data_ptr(), lg.data_ptr(), sp)
+        nxt[sid] = int(tok.item())
+        got[sid].append(lg.cpu().numpy()[0].copy())
+
+    def decode(stages, ids):
+        B = len(ids)
+        x = torch.tensor([nxt[i] for i in ids], dtype=torch.int32, device="cuda")
+        tok = torch.zeros(B, dtype=torch.int32, device="cuda")
+        lg = torch.zeros((B, CFG.vocab), dtype=torch.float32, device="cuda")
+        for st in stages:
+            if st.end == CFG.n_layers:
+                st.decode(ids, x.data_ptr(), tok.data_ptr(), lg.data_ptr(), sp)
+            else:
+                out = torch.zeros((B, CFG.hidden), dtype=torch.bfloat16, device="cuda")
+                st.decode(ids, x.data_ptr(), out.data_ptr(), 0, sp)
+                x = out
+        t, l = tok.cpu().numpy(), lg.cpu().numpy()
+        for k, i in enumerate(ids):
+            nxt[i] = int(t[k])
+            got[i].append(l[k].copy())
+
+    pipe = [s0, s1]
+    prefill(pipe, 11)
+    decode(pipe, [11])
+    decode(pipe, [11])
+    prefill(pipe, 12)                        # joins
+    decode(pipe, [11, 12])
+    decode(pipe, [12, 11])                   # order within a batch does not matter
+    prefill(pipe, 13)                        # joins
+    decode(pipe, [11, 12, 13])
+    for st in pipe:                          # 11 leaves after its last step
+        hs.hs_seq_free(st.h, 11)
+    decode(pipe, [13, 12])
+    hs.hs_stage_merge(s0.h, [s1.h], sp)      # drain and consolidate
+    assert s0.info()["live_seqs"] == 2 and s1.info()["live_seqs"] == 0
+    decode([s0], [12, 13])
+    decode([s0], [12])                       # 13 finished; 12 runs on alone
+    for sid, lgs in got.items():
+        assert len(lgs) == len(ref[sid]), sid
+        assert np.array_equal(np.stack(lgs), ref[sid]), sid
