@@ -21,6 +21,7 @@
 #include "hs_device.h"
 #include "hs_kernels.h"
 
+#include <stdio.h>
 #include <stdlib.h>
 #include <string.h>
 
@@ -628,7 +629,25 @@ hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info) {
   hipError_t e;
   if (a.M <= 64) {
     const int mch = (a.M + 15) / 16;
-    if (epi == EPI_SWIGLU) {
+    // rows per workgroup (16 NF) and 64-k slabs unrolled per wave (U);
+    // HS_SKINNY_CFG="<NF>,<U>" forces a choice for one token chunk (tuning only)
+    static const char* force = getenv("HS_SKINNY_CFG");
+    int nf = epi == EPI_SWIGLU ? 2 : 1, u = 0;
+    // 9-16 tokens: wide projections read more weight rows per activation
+    // fetch (measured on MI355X: gate/up 28672 wide 55 -> 50 us, QKV 6144
+    // wide 17.8 -> 15.3 us at 16 tokens); the 4096-wide ones need the
+    // workgroups more
+    if (mch == 1 && a.M > 8) {
+      if (epi == EPI_SWIGLU && a.N >= 16384) nf = 4, u = 1;
+      else if (epi != EPI_SWIGLU && a.N >= 6144 && a.N <= 12288) nf = 2, u = 4;
+    }
+    if (force && *force) sscanf(force, "%d,%d", &nf, &u);
+    if (epi == EPI_SWIGLU && (nf % 2)) nf = 2;
+    if (mch == 1 && nf == 4 && u == 2) e = dispatch_epi_skinny<4, 1, 2>(a, epi, s);
+    else if (mch == 1 && nf == 4) e = dispatch_epi_skinny<4, 1, 1>(a, epi, s);
+    else if (mch == 1 && nf == 2 && u == 4) e = dispatch_epi_skinny<2, 1, 4>(a, epi, s);
+    else if (mch == 1 && nf == 1 && u == 2) e = dispatch_epi_skinny<1, 1, 2>(a, epi, s);
+    else if (epi == EPI_SWIGLU) {
       switch (mch) {
         case 1: e = dispatch_epi_skinny<2, 1, 2>(a, epi, s); break;
         case 2: e = dispatch_epi_skinny<2, 2, 2>(a, epi, s); break;

@@ -18,7 +18,8 @@ def _hs():
 
 GEMM_SHAPES = [(1, 256, 256), (7, 768, 256), (16, 1376, 256), (33, 512, 688),
                (64, 4096, 4096), (65, 1024, 1024), (200, 768, 256), (512, 1024, 512),
-               (777, 1376, 688), (1024, 4096, 4096)]
+               (777, 1376, 688), (1024, 4096, 4096),
+               (12, 16384, 256), (16, 6144, 512)]   # wide 9-16-token decode variants
 
 
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
