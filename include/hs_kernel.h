@@ -37,6 +37,18 @@ hs_status hs_k_gemm(const void* X, int64_t ldx, const void* W, void* Y, int64_t 
                     const void* R, int64_t ldr, int32_t M, int32_t N, int32_t K, int32_t epi,
                     void* stream);
 
+/* The same product with the RMSNorm of X's rows folded in (the norm of
+ * section 2.1's decoder layer before attention and before the FFN):
+ * Y = epilogue(rmsnorm(X) W^T) with rmsnorm(x) = x / sqrt(mean(x^2) + eps) * g,
+ * g a bf16 [K] gain. X holds the raw rows; every activation is multiplied
+ * by the gain and rounded to bf16 on the way into the product, and each
+ * output row is scaled by its 1 / RMS in float32 afterwards. For decode
+ * batches: requires 1 <= M <= 16 and K % 64 == 0 (HS_EINVAL otherwise);
+ * other arguments, epilogues and the workspace as hs_k_gemm. */
+hs_status hs_k_gemm_rmsnorm(const void* X, int64_t ldx, const void* g, float eps, const void* W,
+                            void* Y, int64_t ldy, const void* R, int64_t ldr, int32_t M,
+                            int32_t N, int32_t K, int32_t epi, void* stream);
+
 /* Causal grouped-query attention over packed sequences (the attention of the
  * prefill pass). qkv: bf16 [T][(n_heads + 2 n_kv_heads) head_dim] holding
  * post-RoPE q, k, v per token; out: bf16 [T][n_heads head_dim]; cu_seqlens:

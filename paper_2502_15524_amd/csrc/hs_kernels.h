@@ -30,6 +30,9 @@ struct GemmArgs {
   // workspace must not overlap in time.
   float* part = nullptr; int64_t part_floats = 0;
   uint32_t* flags = nullptr; int64_t flags_n = 0;
+  // Optional RMSNorm of the rows of X with this gain (M <= 16, K % 64 == 0):
+  // the product is then of rmsnorm(X) * gain, X being the raw rows.
+  const bf16_t* norm_gain = nullptr; float norm_eps = 0.f;
 };
 
 // Describes what was launched (for timing).

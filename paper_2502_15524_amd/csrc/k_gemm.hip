@@ -431,14 +431,20 @@ void gemm_ring(GemmArgs a, GemmSched sc) {
 // blocks are adjacent, so a wave reads 2 KiB per 16 rows contiguously; lane
 // (row fr, group g) takes chunk 4 ks + g of its row for the ks-th 32-k MFMA.
 
-template <int NF, int MCH, int U, int EPI>
-__global__ __launch_bounds__(256) void gemm_skinny(GemmArgs a) {
+// With NORM, X is the un-normalised residual stream and the GEMM applies the
+// RMSNorm of its rows itself: each loaded activation chunk is multiplied by
+// the norm gain (and rounded to bf16 like a stored activation), the squares
+// of the raw values are summed along the way, and the epilogue scales each
+// token's outputs by 1 / sqrt(mean square + eps). Used for decode, where the
+// separate norm kernel would cost a launch per projection.
+template <int NF, int MCH, int U, int EPI, bool NORM, int WV>
+__global__ __launch_bounds__(64 * WV) void gemm_skinny(GemmArgs a) {
   static_assert(EPI != EPI_SWIGLU || (NF % 2) == 0, "SwiGLU needs gate/up tile pairs");
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n0 = blockIdx.x * 16 * NF;
   const int kp = (a.K + 63) & ~63;
   const int nslab = kp / 64;
-  const int sq = (nslab + 3) / 4;  // slabs per wave
+  const int sq = (nslab + WV - 1) / WV;  // slabs per wave
   const int sb = wave * sq, se = min(nslab, sb + sq);
   const int fr = lane & 15, g = lane >> 4;
   const int64_t slab_bytes = (int64_t)(a.N / 8) * 1024;
@@ -460,13 +466,16 @@ __global__ __launch_bounds__(256) void gemm_skinny(GemmArgs a) {
   }
 
   f32x4_v acc[NF][MCH];
+  float ssq[MCH];
 #pragma unroll
   for (int f = 0; f < NF; ++f)
 #pragma unroll
     for (int c = 0; c < MCH; ++c) acc[f][c] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int c = 0; c < MCH; ++c) ssq[c] = 0.f;
 
   for (int s0 = sb; s0 < se; s0 += U) {
-    pack8 wv[NF][U][2], xv[MCH][U][2];
+    pack8 wv[NF][U][2], xv[MCH][U][2], gv[U][2];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int sl = s0 + u;
@@ -482,7 +491,24 @@ __global__ __launch_bounds__(256) void gemm_skinny(GemmArgs a) {
 #pragma unroll
         for (int c = 0; c < MCH; ++c)
           xv[c][u][ks] = (ok && xrow[c]) ? ld16(xrow[c] + sl * 64 + chunk * 8) : zero8();
+        if constexpr (NORM) gv[u][ks] = ok ? ld16(a.norm_gain + sl * 64 + chunk * 8) : zero8();
       }
+    }
+    if constexpr (NORM) {
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+          for (int c = 0; c < MCH; ++c) {
+            pack8& x = xv[c][u][ks];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float x0 = lo_bf(x.w[e]), x1 = hi_bf(x.w[e]);
+              ssq[c] += x0 * x0 + x1 * x1;
+              x.w[e] = pack2bf(x0 * lo_bf(gv[u][ks].w[e]), x1 * hi_bf(gv[u][ks].w[e]));
+            }
+          }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u)
@@ -496,7 +522,17 @@ __global__ __launch_bounds__(256) void gemm_skinny(GemmArgs a) {
                 as_bf16x8(wv[f][u][ks]), as_bf16x8(xv[c][u][ks]), acc[f][c], 0, 0, 0);
   }
 
-  __shared__ f32x4_v red[3][NF][MCH][64];
+  __shared__ f32x4_v red[WV - 1][NF][MCH][64];
+  __shared__ float red_ss[WV][MCH][16];
+  if constexpr (NORM) {
+    // the 4 k-groups of a token (lanes fr, fr+16, fr+32, fr+48), then waves
+#pragma unroll
+    for (int c = 0; c < MCH; ++c) {
+      ssq[c] += __shfl_xor(ssq[c], 16, 64);
+      ssq[c] += __shfl_xor(ssq[c], 32, 64);
+      if (g == 0) red_ss[wave][c][fr] = ssq[c];
+    }
+  }
   if (wave > 0) {
 #pragma unroll
     for (int f = 0; f < NF; ++f)
@@ -506,11 +542,22 @@ __global__ __launch_bounds__(256) void gemm_skinny(GemmArgs a) {
   __syncthreads();
   if (wave != 0) return;
 #pragma unroll
-  for (int w = 0; w < 3; ++w)
+  for (int w = 0; w < WV - 1; ++w)
 #pragma unroll
     for (int f = 0; f < NF; ++f)
 #pragma unroll
       for (int c = 0; c < MCH; ++c) acc[f][c] += red[w][f][c][lane];
+  if constexpr (NORM) {
+#pragma unroll
+    for (int c = 0; c < MCH; ++c) {
+      float tot = red_ss[0][c][fr];
+#pragma unroll
+      for (int w = 1; w < WV; ++w) tot += red_ss[w][c][fr];
+      const float inv = 1.0f / sqrtf(tot / (float)a.K + a.norm_eps);
+#pragma unroll
+      for (int f = 0; f < NF; ++f) acc[f][c] *= inv;
+    }
+  }
 
   const int fq = g * 4;
 #pragma unroll
@@ -531,29 +578,53 @@ __global__ __launch_bounds__(256) void gemm_skinny(GemmArgs a) {
 
 namespace {
 
-template <int NF, int MCH, int U>
-hipError_t dispatch_epi_skinny(const GemmArgs& a, int epi, hipStream_t s) {
+template <int NF, int MCH, int U, int WV, bool NORM>
+hipError_t dispatch_skinny_norm(const GemmArgs& a, int epi, hipStream_t s) {
   const int grid = (a.N + 16 * NF - 1) / (16 * NF);
+  const dim3 blk(64 * WV);
   switch (epi) {
     case EPI_STORE:
-      hipLaunchKernelGGL((gemm_skinny<NF, MCH, U, EPI_STORE>), dim3(grid), dim3(256), 0, s, a);
+      hipLaunchKernelGGL((gemm_skinny<NF, MCH, U, EPI_STORE, NORM, WV>), dim3(grid), blk, 0, s, a);
       break;
     case EPI_RESID:
-      hipLaunchKernelGGL((gemm_skinny<NF, MCH, U, EPI_RESID>), dim3(grid), dim3(256), 0, s, a);
+      hipLaunchKernelGGL((gemm_skinny<NF, MCH, U, EPI_RESID, NORM, WV>), dim3(grid), blk, 0, s, a);
       break;
     case EPI_SWIGLU:
       if constexpr (NF % 2 == 0) {
-        hipLaunchKernelGGL((gemm_skinny<NF, MCH, U, EPI_SWIGLU>), dim3(grid), dim3(256), 0, s, a);
+        hipLaunchKernelGGL((gemm_skinny<NF, MCH, U, EPI_SWIGLU, NORM, WV>), dim3(grid), blk, 0, s, a);
         break;
       } else {
         return hipErrorInvalidValue;
       }
     case EPI_F32:
-      hipLaunchKernelGGL((gemm_skinny<NF, MCH, U, EPI_F32>), dim3(grid), dim3(256), 0, s, a);
+      hipLaunchKernelGGL((gemm_skinny<NF, MCH, U, EPI_F32, NORM, WV>), dim3(grid), blk, 0, s, a);
       break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+template <int NF, int MCH, int U, int WV>
+hipError_t dispatch_epi_skinny(const GemmArgs& a, int epi, hipStream_t s) {
+  if (a.norm_gain) {
+    // the fused norm is only built for one 16-token chunk (decode batches)
+    if constexpr (MCH == 1) return dispatch_skinny_norm<NF, 1, U, WV, true>(a, epi, s);
+    else return hipErrorInvalidValue;
+  }
+  return dispatch_skinny_norm<NF, MCH, U, WV, false>(a, epi, s);
+}
+
+// The skinny variants built for one 16-token chunk, as (rows per workgroup /
+// 16, slabs unrolled per wave, waves per workgroup): the ones the selection
+// in gemm() takes.
+#define HS_SKINNY_MCH1(X) X(1, 4, 4) X(1, 1, 8) X(1, 2, 8) X(2, 1, 4) X(2, 1, 8) X(4, 1, 4)
+
+hipError_t dispatch_skinny1(const GemmArgs& a, int epi, int nf, int u, int wv, hipStream_t s) {
+#define HS_SKINNY_CASE(NF_, U_, WV_) \
+  if (nf == NF_ && u == U_ && wv == WV_) return dispatch_epi_skinny<NF_, 1, U_, WV_>(a, epi, s);
+  HS_SKINNY_MCH1(HS_SKINNY_CASE)
+#undef HS_SKINNY_CASE
+  return hipErrorInvalidValue;
 }
 
 template <int BN, int BM, int NS, int SPR, bool SK>
@@ -616,6 +687,8 @@ hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info) {
   if (epi == EPI_SWIGLU && (a.N % 32)) return hipErrorInvalidValue;
   if (epi == EPI_RESID && (!a.R || (a.ldr % 4))) return hipErrorInvalidValue;
   if (((uintptr_t)a.X | (uintptr_t)a.W | (uintptr_t)a.Y) & 15) return hipErrorInvalidValue;
+  if (a.norm_gain && (a.M > 16 || (a.K % 64) || ((uintptr_t)a.norm_gain & 15)))
+    return hipErrorInvalidValue;
   // 32-bit byte offsets in the buffer loads
   if ((uint64_t)a.N * kp * 2 >= (1ull << 31) || (uint64_t)a.M * a.ldx * 2 >= (1ull << 31))
     return hipErrorInvalidValue;
@@ -629,40 +702,45 @@ hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info) {
   hipError_t e;
   if (a.M <= 64) {
     const int mch = (a.M + 15) / 16;
-    // rows per workgroup (16 NF) and 64-k slabs unrolled per wave (U);
-    // HS_SKINNY_CFG="<NF>,<U>" forces a choice for one token chunk (tuning only)
+    // Rows per workgroup (16 NF), 64-k slabs unrolled per wave (U) and waves
+    // per workgroup (WV) for one token chunk, from a sweep on MI355X over the
+    // decode projections of 7B, 8B and 13B models at 1, 8 and 16 tokens:
+    // narrow outputs (o, down, QKV up to 8192 wide) fill the chip with eight
+    // waves per workgroup, wide ones (QKV, gate/up) with four; above 8 tokens
+    // wide gate/up reads more rows per activation fetch, and so do o/down
+    // above 4 tokens when one row tile per CU does not cover them (5120
+    // wide: 40.3 instead of 55.0 us at 16 tokens). WV depends on the
+    // shape only, never on M, so that a token's result (its k order) does not
+    // depend on how many tokens share the call.
+    // HS_SKINNY_CFG="<NF>,<U>,<WV>" forces a choice (tuning only).
     static const char* force = getenv("HS_SKINNY_CFG");
-    int nf = epi == EPI_SWIGLU ? 2 : 1, u = 0;
-    // 9-16 tokens: wide projections read more weight rows per activation
-    // fetch (measured on MI355X: gate/up 28672 wide 55 -> 50 us, QKV 6144
-    // wide 17.8 -> 15.3 us at 16 tokens); the 4096-wide ones need the
-    // workgroups more
-    if (mch == 1 && a.M > 8) {
-      if (epi == EPI_SWIGLU && a.N >= 16384) nf = 4, u = 1;
-      else if (epi != EPI_SWIGLU && a.N >= 6144 && a.N <= 12288) nf = 2, u = 4;
+    int nf = 1, u = 4, wv = 4;  // LM head
+    if (epi == EPI_SWIGLU) {
+      nf = (a.M > 8 && a.N >= 16384) ? 4 : 2, u = 1;
+    } else if (epi == EPI_RESID) {
+      if (a.M > 4 && a.N / 16 > device_cus()) nf = 2, u = 1, wv = 8;
+      else nf = 1, u = a.M <= 8 ? 2 : 1, wv = 8;
+    } else if (epi == EPI_STORE) {
+      nf = 2, u = 1, wv = a.N <= 8192 ? 8 : 4;
     }
-    if (force && *force) sscanf(force, "%d,%d", &nf, &u);
+    if (force && *force) sscanf(force, "%d,%d,%d", &nf, &u, &wv);
     if (epi == EPI_SWIGLU && (nf % 2)) nf = 2;
-    if (mch == 1 && nf == 4 && u == 2) e = dispatch_epi_skinny<4, 1, 2>(a, epi, s);
-    else if (mch == 1 && nf == 4) e = dispatch_epi_skinny<4, 1, 1>(a, epi, s);
-    else if (mch == 1 && nf == 2 && u == 4) e = dispatch_epi_skinny<2, 1, 4>(a, epi, s);
-    else if (mch == 1 && nf == 1 && u == 2) e = dispatch_epi_skinny<1, 1, 2>(a, epi, s);
-    else if (epi == EPI_SWIGLU) {
+    if (mch == 1) {
+      e = dispatch_skinny1(a, epi, nf, u, wv, s);
+    } else if (epi == EPI_SWIGLU) {
       switch (mch) {
-        case 1: e = dispatch_epi_skinny<2, 1, 2>(a, epi, s); break;
-        case 2: e = dispatch_epi_skinny<2, 2, 2>(a, epi, s); break;
-        case 3: e = dispatch_epi_skinny<2, 3, 1>(a, epi, s); break;
-        default: e = dispatch_epi_skinny<2, 4, 1>(a, epi, s); break;
+        case 2: e = dispatch_epi_skinny<2, 2, 2, 4>(a, epi, s); break;
+        case 3: e = dispatch_epi_skinny<2, 3, 1, 4>(a, epi, s); break;
+        default: e = dispatch_epi_skinny<2, 4, 1, 4>(a, epi, s); break;
       }
     } else {
       switch (mch) {
-        case 1: e = dispatch_epi_skinny<1, 1, 4>(a, epi, s); break;
-        case 2: e = dispatch_epi_skinny<1, 2, 2>(a, epi, s); break;
-        case 3: e = dispatch_epi_skinny<1, 3, 2>(a, epi, s); break;
-        default: e = dispatch_epi_skinny<1, 4, 1>(a, epi, s); break;
+        case 2: e = dispatch_epi_skinny<1, 2, 2, 4>(a, epi, s); break;
+        case 3: e = dispatch_epi_skinny<1, 3, 2, 4>(a, epi, s); break;
+        default: e = dispatch_epi_skinny<1, 4, 1, 4>(a, epi, s); break;
       }
     }
-    snprintf(name, sizeof name, "gemm_skinny_%s", kEpiName[epi]);
+    snprintf(name, sizeof name, "gemm_skinny_%s%s", a.norm_gain ? "norm_" : "", kEpiName[epi]);
   } else {
     // Configuration by a small cost model: a data-parallel launch takes
     // rounds x (tile flops / per-CU rate of its tile shape); a stream-K launch

@@ -53,6 +53,17 @@ hs_status launched(hipError_t e, const char* what) {
 }
 }  // namespace
 
+hs_status gemm_call(GemmArgs a, int32_t epi, void* stream) {
+  GemmWs* ws = nullptr;
+  const hs_status r = gemm_ws(&ws);
+  if (r != HS_OK) return r;
+  a.part = ws->part;
+  a.part_floats = kWsPartFloats;
+  a.flags = ws->flags;
+  a.flags_n = kWsFlags;
+  return launched(gemm(a, epi, static_cast<hipStream_t>(stream), nullptr), "gemm");
+}
+
 extern "C" hs_status hs_k_gemm(const void* X, int64_t ldx, const void* Wt, void* Y, int64_t ldy,
                                const void* R, int64_t ldr, int32_t M, int32_t N, int32_t K,
                                int32_t epi, void* stream) {
@@ -60,14 +71,24 @@ extern "C" hs_status hs_k_gemm(const void* X, int64_t ldx, const void* Wt, void*
     if (!X || !Wt || !Y) return fail(HS_EINVAL, "null operand");
     GemmArgs a{static_cast<const bf16_t*>(X), ldx, static_cast<const bf16_t*>(Wt), Y, ldy,
                static_cast<const bf16_t*>(R), ldr, M, N, K};
-    GemmWs* ws = nullptr;
-    const hs_status r = gemm_ws(&ws);
-    if (r != HS_OK) return r;
-    a.part = ws->part;
-    a.part_floats = kWsPartFloats;
-    a.flags = ws->flags;
-    a.flags_n = kWsFlags;
-    return launched(gemm(a, epi, static_cast<hipStream_t>(stream), nullptr), "gemm");
+    return gemm_call(a, epi, stream);
+  } catch (...) {
+    return fail(HS_EINVAL, "unexpected internal error");
+  }
+}
+
+extern "C" hs_status hs_k_gemm_rmsnorm(const void* X, int64_t ldx, const void* g, float eps,
+                                       const void* Wt, void* Y, int64_t ldy, const void* R,
+                                       int64_t ldr, int32_t M, int32_t N, int32_t K, int32_t epi,
+                                       void* stream) {
+  try {
+    if (!X || !g || !Wt || !Y) return fail(HS_EINVAL, "null operand");
+    if (M < 1 || M > 16 || K % 64) return fail(HS_EINVAL, "needs 1 <= M <= 16 and K % 64 == 0");
+    GemmArgs a{static_cast<const bf16_t*>(X), ldx, static_cast<const bf16_t*>(Wt), Y, ldy,
+               static_cast<const bf16_t*>(R), ldr, M, N, K};
+    a.norm_gain = static_cast<const bf16_t*>(g);
+    a.norm_eps = eps;
+    return gemm_call(a, epi, stream);
   } catch (...) {
     return fail(HS_EINVAL, "unexpected internal error");
   }

@@ -396,13 +396,21 @@ hs_status layer_forward(hs_stage* st, int l, bf16_t* x, const LayerCall& c, hipS
   const int H = m.hidden, D = m.head_dim, F = m.ffn;
   const int FA = (int)round64(F);  // activation row stride: zero columns up to a multiple of 64
   const int NQKV = (m.n_heads + 2 * m.n_kv_heads) * D, QD = m.n_heads * D;
+  // Up to 16 tokens (decode batches) the skinny GEMMs apply the two norms
+  // themselves and read the residual stream directly.
+  const bool fuse_norm = c.T <= 16;
   hs_status r;
-  r = run(st, s, "attn_norm", [&](LaunchInfo* i) {
-    return rmsnorm(x, H, nullptr, c.T, H, W(st, ls.attn_norm), m.rms_eps, st->w_u, H, s, i);
-  });
-  if (r != HS_OK) return r;
+  if (!fuse_norm) {
+    r = run(st, s, "attn_norm", [&](LaunchInfo* i) {
+      return rmsnorm(x, H, nullptr, c.T, H, W(st, ls.attn_norm), m.rms_eps, st->w_u, H, s, i);
+    });
+    if (r != HS_OK) return r;
+  }
   r = run(st, s, "qkv", [&](LaunchInfo* i) {
-    GemmArgs g = gemm_args(st, st->w_u, H, W(st, ls.qkv), st->w_qkv, NQKV, nullptr, 0, c.T, NQKV, H);
+    GemmArgs g = fuse_norm
+                     ? gemm_args(st, x, H, W(st, ls.qkv), st->w_qkv, NQKV, nullptr, 0, c.T, NQKV, H)
+                     : gemm_args(st, st->w_u, H, W(st, ls.qkv), st->w_qkv, NQKV, nullptr, 0, c.T, NQKV, H);
+    if (fuse_norm) g.norm_gain = W(st, ls.attn_norm), g.norm_eps = m.rms_eps;
     return gemm(g, EPI_STORE, s, i);
   });
   if (r != HS_OK) return r;
@@ -435,12 +443,17 @@ hs_status layer_forward(hs_stage* st, int l, bf16_t* x, const LayerCall& c, hipS
     return gemm(g, EPI_RESID, s, i);
   });
   if (r != HS_OK) return r;
-  r = run(st, s, "ffn_norm", [&](LaunchInfo* i) {
-    return rmsnorm(x, H, nullptr, c.T, H, W(st, ls.ffn_norm), m.rms_eps, st->w_u, H, s, i);
-  });
-  if (r != HS_OK) return r;
+  if (!fuse_norm) {
+    r = run(st, s, "ffn_norm", [&](LaunchInfo* i) {
+      return rmsnorm(x, H, nullptr, c.T, H, W(st, ls.ffn_norm), m.rms_eps, st->w_u, H, s, i);
+    });
+    if (r != HS_OK) return r;
+  }
   r = run(st, s, "gate_up", [&](LaunchInfo* i) {
-    GemmArgs g = gemm_args(st, st->w_u, H, W(st, ls.gateup), st->w_act, FA, nullptr, 0, c.T, 2 * F, H);
+    GemmArgs g = fuse_norm
+                     ? gemm_args(st, x, H, W(st, ls.gateup), st->w_act, FA, nullptr, 0, c.T, 2 * F, H)
+                     : gemm_args(st, st->w_u, H, W(st, ls.gateup), st->w_act, FA, nullptr, 0, c.T, 2 * F, H);
+    if (fuse_norm) g.norm_gain = W(st, ls.ffn_norm), g.norm_eps = m.rms_eps;
     return gemm(g, EPI_SWIGLU, s, i);
   });
   if (r != HS_OK) return r;

@@ -112,6 +112,8 @@ _SIGS = {
     "hs_pack_tiled": [_P, C.c_int64, C.c_int64, _P],
     "hs_k_attn_prefill": [_P, _P, C.POINTER(C.c_int32), C.c_int32, C.c_int32, C.c_int32,
                           C.c_int32, _P],
+    "hs_k_gemm_rmsnorm": [_P, C.c_int64, _P, C.c_float, _P, _P, C.c_int64, _P, C.c_int64,
+                          C.c_int32, C.c_int32, C.c_int32, C.c_int32, _P],
     "hs_k_rmsnorm": [_P, _P, _P, C.c_int32, C.c_int32, C.c_float, _P],
     "hs_k_attn_decode": [_P, C.c_int64, _P, _P, _P, _P, C.c_int64, C.c_int32, C.c_int32,
                          C.c_int32, C.c_int32, C.c_int32, C.c_int32, _P],
@@ -342,6 +344,13 @@ def hs_k_gemm(X, ldx, W, Y, ldy, R, ldr, M, N, K, epi, stream=0):
     if isinstance(epi, str):
         epi = EPI[epi]
     _check(lib().hs_k_gemm(X, ldx, W, Y, ldy, R or None, ldr, M, N, K, epi, stream or None))
+
+
+def hs_k_gemm_rmsnorm(X, ldx, g, eps, W, Y, ldy, R, ldr, M, N, K, epi, stream=0):
+    if isinstance(epi, str):
+        epi = EPI[epi]
+    _check(lib().hs_k_gemm_rmsnorm(X, ldx, g, eps, W, Y, ldy, R or None, ldr, M, N, K, epi,
+                                   stream or None))
 
 
 def hs_pack_tiled(src_ptr, rows, cols, dst_ptr):

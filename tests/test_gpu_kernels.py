@@ -19,7 +19,8 @@ def _hs():
 GEMM_SHAPES = [(1, 256, 256), (7, 768, 256), (16, 1376, 256), (33, 512, 688),
                (64, 4096, 4096), (65, 1024, 1024), (200, 768, 256), (512, 1024, 512),
                (777, 1376, 688), (1024, 4096, 4096),
-               (12, 16384, 256), (16, 6144, 512)]   # wide 9-16-token decode variants
+               (12, 16384, 256), (16, 6144, 512),   # wide 9-16-token decode variants
+               (3, 2048, 11008), (14, 1024, 5120)]  # eight-wave splits of a long k
 
 
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
@@ -217,6 +218,77 @@ def test_rmsnorm(rows, hidden):
     torch.cuda.synchronize()
     ref = rms_norm(x.astype(np.float64), g.astype(np.float64), 1e-5)
     assert np.max(np.abs(G.from_dev_bf16(out) - ref)) <= 8e-3 * np.abs(ref).max()
+
+
+# Decode projections with the RMSNorm folded in, one shape per skinny
+# variant the stage reaches (7B QKV and gate/up at 1, 8, 12 and 16 tokens)
+# plus small ragged ones; rows carry different scales so that a wrong
+# per-row 1/RMS shows.
+@pytest.mark.parametrize("M,N,K,epi", [
+    (1, 12288, 4096, "store"), (8, 22016, 4096, "swiglu"), (16, 28672, 4096, "swiglu"),
+    (12, 6144, 4096, "store"), (16, 12288, 4096, "store"), (5, 1536, 256, "resid"),
+    (3, 512, 64, "f32"), (16, 1376, 320, "swiglu")])
+def test_gemm_rmsnorm(M, N, K, epi):
+    torch = G.torch()
+    hs = _hs()
+    rng = np.random.default_rng(M * 13 + N + K)
+    scale = 10.0 ** (np.arange(M) % 3 - 1)[:, None]
+    X = gen.round_to_bf16((rng.standard_normal((M, K)) * scale).astype(np.float32))
+    g = gen.round_to_bf16((1 + 0.3 * rng.standard_normal(K)).astype(np.float32))
+    Wt = gen.round_to_bf16((rng.standard_normal((N, K)) * 0.02).astype(np.float32))
+    u = rms_norm(X.astype(np.float64), g.astype(np.float64), 1e-5)
+    acc = u @ Wt.astype(np.float64).T
+    ncol = N // 2 if epi == "swiglu" else N
+    R = gen.round_to_bf16(rng.standard_normal((M, ncol)).astype(np.float32))
+    if epi == "swiglu":
+        idx = np.arange(ncol)
+        ref = silu(acc[:, (idx // 16) * 32 + idx % 16]) * acc[:, (idx // 16) * 32 + 16 + idx % 16]
+    elif epi == "resid":
+        ref = R + acc
+    else:
+        ref = acc
+    dX, dg = G.to_dev_bf16(X), G.to_dev_bf16(g)
+    dW = torch.from_numpy(G.tile_bits(gen.to_bf16_bits(Wt)).view(np.int16)).cuda()
+    outs = []
+    for _ in range(2):
+        if epi == "f32":
+            Y = torch.zeros((M, N), dtype=torch.float32, device="cuda")
+        elif epi == "resid":
+            Y = G.to_dev_bf16(R)
+        else:
+            Y = torch.zeros((M, ncol), dtype=torch.bfloat16, device="cuda")
+        hs.hs_k_gemm_rmsnorm(dX.data_ptr(), K, dg.data_ptr(), 1e-5, dW.data_ptr(), Y.data_ptr(),
+                             ncol, Y.data_ptr() if epi == "resid" else 0, ncol, M, N, K, epi,
+                             G.stream_ptr())
+        torch.cuda.synchronize()
+        outs.append(Y.cpu().numpy() if epi == "f32" else G.from_dev_bf16(Y))
+    assert np.array_equal(outs[0], outs[1])
+    # per row: the bf16 rounding of the normalised activations dominates
+    for m in range(M):
+        err = np.abs(outs[0][m] - ref[m]).max()
+        assert err <= 8e-3 * np.abs(ref[m]).max() + 1e-6, (m, err)
+    # the fused norm does not depend on the other rows of the batch
+    if M > 1:
+        Y1 = torch.zeros((1, N), dtype=torch.float32, device="cuda") if epi == "f32" else (
+            G.to_dev_bf16(R[-1:]) if epi == "resid" else
+            torch.zeros((1, ncol), dtype=torch.bfloat16, device="cuda"))
+        hs.hs_k_gemm_rmsnorm(dX[-1:].data_ptr(), K, dg.data_ptr(), 1e-5, dW.data_ptr(),
+                             Y1.data_ptr(), ncol, Y1.data_ptr() if epi == "resid" else 0, ncol,
+                             1, N, K, epi, G.stream_ptr())
+        torch.cuda.synchronize()
+        last = Y1.cpu().numpy() if epi == "f32" else G.from_dev_bf16(Y1)
+        assert np.array_equal(last[0], outs[0][-1])
+
+
+def test_gemm_rmsnorm_rejects_unsupported_shapes():
+    torch = G.torch()
+    hs = _hs()
+    buf = torch.zeros(1 << 16, dtype=torch.bfloat16, device="cuda")
+    p = buf.data_ptr()
+    for (M, N, K) in ((17, 64, 64), (0, 64, 64), (4, 64, 72)):
+        with pytest.raises(hs.HSError) as e:
+            hs.hs_k_gemm_rmsnorm(p, 128, p, 1e-5, p, p, N, 0, 0, M, N, K, 0)
+        assert e.value.code == hs.HS_EINVAL
 
 
 def test_gemm_rejects_unsupported_shapes():
