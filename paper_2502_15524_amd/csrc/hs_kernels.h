@@ -89,8 +89,7 @@ struct AttnDecodeArgs {
   int B, n_heads, n_kv_heads, D, max_blocks, max_splits, call_splits;
   double kv_bytes;                // bytes of K/V read, for reporting
 };
-hipError_t attn_decode(const AttnDecodeArgs& a, hipStream_t s, LaunchInfo* info_split,
-                       LaunchInfo* info_combine);
+hipError_t attn_decode(const AttnDecodeArgs& a, hipStream_t s, LaunchInfo* info);
 
 // Greedy token per row: lowest index of the row's maximum. part: scratch of
 // n_rows * argmax_chunks(n_cols) * 2 int32.

@@ -219,10 +219,13 @@ int attn_prefill_waves(int64_t tiles_of_128, int n_heads) {
 // group of 4 tokens a thread forms the G scores (partial dot products summed
 // over the token's lanes with DPP row operations), then updates its online
 // softmax once: new max, one rescale of the accumulators, four
-// probabilities. The token slots are merged through LDS in a fixed order.
-// Output per split and query head: the unnormalised P V, the max score
-// (log2 domain) and the sum of exp2(score - max); the combine kernel merges
-// the splits in order.
+// probabilities. The token slots of a wave are merged with cross-row lane
+// swaps, the four waves through LDS, in a fixed order.
+//
+// Each split leaves, per query head, the unnormalised P V, the max score
+// (log2 domain) and the sum of exp2(score - max); a second kernel merges
+// the splits in split order with a running max, so the result does not
+// depend on which split ends when.
 
 // Sum over the 16 lanes of a DPP row (all lanes get the sum). Each step adds
 // a lane permutation that pairs lanes holding disjoint partial sums.
@@ -241,6 +244,65 @@ __device__ __forceinline__ float row8_sum(float v) {
   return v;
 }
 
+// Lanes i and i ^ 8 of each row (row_ror:8), rows 2k and 2k + 1
+// (permlane16 swap) and the two halves of the wave (permlane32 swap): the
+// operands reach every lane of a group in the same order, so all of them get
+// the same bits.
+__device__ __forceinline__ float xor8_val(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x128, 0xF, 0xF, true));
+}
+template <typename Op>
+__device__ __forceinline__ float rows_pair(float v, Op op) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return op(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+template <typename Op>
+__device__ __forceinline__ float halves_pair(float v, Op op) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return op(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+// op over the token slots of a wave (lanes c + LPT j, j = 0 .. 64 / LPT - 1)
+template <int LPT, typename Op>
+__device__ __forceinline__ float over_slots(float v, Op op) {
+  if constexpr (LPT == 8) v = op(v, xor8_val(v));
+  return halves_pair(rows_pair(v, op), op);
+}
+
+constexpr int kRawBuffer = 0x00020000;   // raw buffer, 32-bit data format
+__device__ __forceinline__ float ld_part(__amdgpu_buffer_rsrc_t r, int byte_off) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, byte_off, 0, 0));
+}
+
+// Merge the n_splits partials of one query head (row r of ro / rml holds
+// split r) in split order with a running max; 8 splits are loaded together.
+template <int D>
+__device__ __forceinline__ float merge_splits(__amdgpu_buffer_rsrc_t ro, __amdgpu_buffer_rsrc_t rml,
+                                              int row0, int n_splits, int d) {
+  float M = -INFINITY, L = 0.f, O = 0.f;
+  for (int s0 = 0; s0 < n_splits; s0 += 8) {
+    float ms[8], ls[8], os[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {  // past the last split: re-read it, then ignore
+      const int row = row0 + min(s0 + u, n_splits - 1);
+      ms[u] = ld_part(rml, row * 8);
+      ls[u] = ld_part(rml, row * 8 + 4);
+      os[u] = ld_part(ro, (row * D + d) * 4);
+    }
+    // branch-free, so that all 24 loads are in flight together; a skipped
+    // split leaves O and L exactly as they were (x 1 + finite x 0)
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const bool ok = s0 + u < n_splits && ms[u] != -INFINITY;
+      const float mn = ok ? fmaxf(M, ms[u]) : M;
+      const float wo = ok ? fast_exp2(M - mn) : 1.f, wn = ok ? fast_exp2(ms[u] - mn) : 0.f;
+      O = O * wo + os[u] * wn;
+      L = L * wo + ls[u] * wn;
+      M = mn;
+    }
+  }
+  return O / L;
+}
+
 template <int D, int G>
 __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a, float scale_log2) {
   constexpr int LPT = D / 8;        // lanes per token
@@ -249,16 +311,25 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a
   constexpr int UNR = PASSES < 4 ? PASSES : 4;
   static_assert(PASSES % UNR == 0, "split/pass mismatch");
   static_assert(LPT == 16 || LPT == 8, "head dim 128 or 64");
-  __shared__ float s_ml[TPP][G][2];
-  __shared__ float s_acc[TPP][G][D];
+  static_assert(TPP == 16 || TPP == 32, "one or two cache blocks per pass");
+  constexpr int BPS = kDecodeSplit / 16;  // cache blocks per split
+  static_assert(BPS == 4, "split of four cache blocks");
+  __shared__ float s_ml[4][G][2];
+  __shared__ float s_acc[4][G][D];
 
   const int split = blockIdx.x, kh = blockIdx.y, b = blockIdx.z;
+  // the split's block-table entries are loaded together with the context
+  // length: one round trip before the key/value loads instead of two
+  const int32_t* bt = a.block_table + (int64_t)b * a.max_blocks;
+  int phys[BPS];
+#pragma unroll
+  for (int j = 0; j < BPS; ++j) phys[j] = bt[min(split * BPS + j, a.max_blocks - 1)];  // past: unused
   const int ctx = a.ctx[b];
+  asm volatile("" ::"s"(phys[0]), "s"(phys[1]), "s"(phys[2]), "s"(phys[3]));  // not sunk below the branch
   const int t_begin = split * kDecodeSplit;
   if (t_begin >= ctx) return;  // uniform across the workgroup
   const int tid = threadIdx.x, tl = tid / LPT, c = tid % LPT;
   const int h0 = kh * G;
-  const int32_t* bt = a.block_table + (int64_t)b * a.max_blocks;
   const int64_t kv_stride = (int64_t)a.n_kv_heads * 16 * D;  // K block -> V block
 
   // all key and value loads of the split go out first
@@ -269,8 +340,8 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a
     kv[p] = zero8();
     vv[p] = zero8();
     if (tok < ctx) {
-      const int phys = bt[tok >> 4];
-      const bf16_t* kp = a.pool + ((int64_t)phys * 2 * a.n_kv_heads + kh) * 16 * D +
+      const int ph = TPP == 16 ? phys[p] : ((tl >> 4) ? phys[2 * p + 1] : phys[2 * p]);
+      const bf16_t* kp = a.pool + ((int64_t)ph * 2 * a.n_kv_heads + kh) * 16 * D +
                          (tok & 15) * D + c * 8;
       kv[p] = ld16(kp);
       vv[p] = ld16(kp + kv_stride);
@@ -286,6 +357,11 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a
       q[gg][2 * e + 1] = hi_bf(v.w[e]);
     }
   }
+  const int wave = tid >> 6;
+  const auto fmax_op = [](float x, float y) { return fmaxf(x, y); };
+  const auto add_op = [](float x, float y) { return x + y; };
+  // partials of this (sequence, kv head): [G][max_splits][D] and [G][max_splits][2]
+  const int64_t base = ((int64_t)b * a.n_heads + h0) * a.max_splits;
 
   {
     float m[G], l[G], acc[G][8];
@@ -341,66 +417,59 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a
       }
     }
 
+    // token slots of the wave -> one (lanes 0 .. LPT - 1 keep it)
 #pragma unroll
     for (int gg = 0; gg < G; ++gg) {
+      const float M = over_slots<LPT>(m[gg], fmax_op);
+      const float w = m[gg] == -INFINITY ? 0.f : fast_exp2(m[gg] - M);
+      const float L = over_slots<LPT>(l[gg] * w, add_op);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) s_acc[tl][gg][c * 8 + e] = acc[gg][e];
-      if (c == 0) {
-        s_ml[tl][gg][0] = m[gg];
-        s_ml[tl][gg][1] = l[gg];
+      for (int e = 0; e < 8; ++e) acc[gg][e] = over_slots<LPT>(acc[gg][e] * w, add_op);
+      if (tid % 64 < LPT) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s_acc[wave][gg][c * 8 + e] = acc[gg][e];
+        if (c == 0) {
+          s_ml[wave][gg][0] = M;
+          s_ml[wave][gg][1] = L;
+        }
       }
     }
     __syncthreads();
     for (int i = tid; i < G * D; i += 256) {
       const int gg = i / D, d = i % D;
       float M = -INFINITY;
-      for (int t = 0; t < TPP; ++t) M = fmaxf(M, s_ml[t][gg][0]);
+#pragma unroll
+      for (int w = 0; w < 4; ++w) M = fmaxf(M, s_ml[w][gg][0]);
       float L = 0.f, O = 0.f;
-      for (int t = 0; t < TPP; ++t) {
-        const float mt = s_ml[t][gg][0];
-        if (mt == -INFINITY) continue;
-        const float w = fast_exp2(mt - M);
-        L += s_ml[t][gg][1] * w;
-        O += s_acc[t][gg][d] * w;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float mw = s_ml[w][gg][0];
+        if (mw == -INFINITY) continue;
+        const float f = fast_exp2(mw - M);
+        L += s_ml[w][gg][1] * f;
+        O += s_acc[w][gg][d] * f;
       }
-      const int64_t idx = ((int64_t)b * a.n_heads + h0 + gg) * a.max_splits + split;
-      a.part_o[idx * D + d] = O;
+      const int64_t row = base + gg * a.max_splits + split;
+      a.part_o[row * D + d] = O;
       if (d == 0) {
-        a.part_ml[idx * 2] = M;
-        a.part_ml[idx * 2 + 1] = L;
+        a.part_ml[row * 2] = M;
+        a.part_ml[row * 2 + 1] = L;
       }
     }
   }
 }
 
-// Merge the splits of one (head, sequence) in split order with a running
-// max; the partials of 8 splits are loaded together.
+// Merge of the splits of every (query head, sequence).
 template <int D>
 __global__ __launch_bounds__(D) void attn_decode_combine_kernel(AttnDecodeArgs a) {
   const int h = blockIdx.x, b = blockIdx.y, d = threadIdx.x;
   const int n_splits = (a.ctx[b] + kDecodeSplit - 1) / kDecodeSplit;
   const int64_t base = ((int64_t)b * a.n_heads + h) * a.max_splits;
-  float M = -INFINITY, L = 0.f, O = 0.f;
-  for (int s0 = 0; s0 < n_splits; s0 += 8) {
-    float ms[8], ls[8], os[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const bool ok = s0 + u < n_splits;
-      ms[u] = ok ? a.part_ml[(base + s0 + u) * 2] : -INFINITY;
-      ls[u] = ok ? a.part_ml[(base + s0 + u) * 2 + 1] : 0.f;
-      os[u] = ok ? a.part_o[(base + s0 + u) * D + d] : 0.f;
-    }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      if (ms[u] == -INFINITY) continue;
-      const float mn = fmaxf(M, ms[u]);
-      const float wo = fast_exp2(M - mn), wn = fast_exp2(ms[u] - mn);
-      O = O * wo + os[u] * wn;
-      L = L * wo + ls[u] * wn;
-      M = mn;
-    }
-  }
-  a.out[(int64_t)b * a.ldo + h * D + d] = f2bf(O / L);
+  const __amdgpu_buffer_rsrc_t ro =
+      __builtin_amdgcn_make_buffer_rsrc(a.part_o + base * D, 0, a.max_splits * D * 4, kRawBuffer);
+  const __amdgpu_buffer_rsrc_t rml =
+      __builtin_amdgcn_make_buffer_rsrc(a.part_ml + base * 2, 0, a.max_splits * 8, kRawBuffer);
+  a.out[(int64_t)b * a.ldo + h * D + d] = f2bf(merge_splits<D>(ro, rml, 0, n_splits, d));
 }
 
 namespace {
@@ -421,11 +490,12 @@ hipError_t launch_split_g(const AttnDecodeArgs& a, int G, float sl, hipStream_t 
 }
 }  // namespace
 
-hipError_t attn_decode(const AttnDecodeArgs& a, hipStream_t s, LaunchInfo* info_split,
-                       LaunchInfo* info_combine) {
+hipError_t attn_decode(const AttnDecodeArgs& a, hipStream_t s, LaunchInfo* info) {
   if (a.B <= 0) return hipSuccess;
   if ((a.D != 64 && a.D != 128) || a.n_kv_heads <= 0 || a.n_heads % a.n_kv_heads) return hipErrorInvalidValue;
   if (a.call_splits <= 0 || a.call_splits > a.max_splits || (a.ldq % 8)) return hipErrorInvalidValue;
+  // byte offsets of one (query head, sequence)'s partials fit 32 bits
+  if ((int64_t)a.max_splits * a.D * 4 >= (1ll << 31)) return hipErrorInvalidValue;
   const int G = a.n_heads / a.n_kv_heads;
   const float sl = (float)(1.4426950408889634 / sqrt((double)a.D));
   hipError_t e = a.D == 128 ? launch_split_g<128>(a, G, sl, s) : launch_split_g<64>(a, G, sl, s);
@@ -435,15 +505,10 @@ hipError_t attn_decode(const AttnDecodeArgs& a, hipStream_t s, LaunchInfo* info_
     hipLaunchKernelGGL(attn_decode_combine_kernel<128>, grid, dim3(128), 0, s, a);
   else
     hipLaunchKernelGGL(attn_decode_combine_kernel<64>, grid, dim3(64), 0, s, a);
-  if (info_split) {
-    info_split->name = "attn_decode_split";
-    info_split->flops = 0;
-    info_split->bytes = a.kv_bytes;
-  }
-  if (info_combine) {
-    info_combine->name = "attn_decode_combine";
-    info_combine->flops = 0;
-    info_combine->bytes = 0;
+  if (info) {
+    info->name = "attn_decode";
+    info->flops = 0;
+    info->bytes = a.kv_bytes;
   }
   return hipGetLastError();
 }

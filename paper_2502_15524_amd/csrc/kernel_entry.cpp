@@ -174,7 +174,7 @@ extern "C" hs_status hs_k_attn_decode(const void* q, int64_t ldq, const void* po
                      block_table, ctx, w.buf, w.buf + (int64_t)B * n_heads * max_splits * head_dim,
                      static_cast<bf16_t*>(out), ldo, B, n_heads, n_kv_heads, head_dim, max_blocks,
                      max_splits, max_splits, 0.0};
-    return launched(attn_decode(a, static_cast<hipStream_t>(stream), nullptr, nullptr),
+    return launched(attn_decode(a, static_cast<hipStream_t>(stream), nullptr),
                     "attn_decode");
   } catch (...) {
     return fail(HS_EINVAL, "unexpected internal error");

@@ -432,9 +432,7 @@ hs_status layer_forward(hs_stage* st, int l, bf16_t* x, const LayerCall& c, hipS
       AttnDecodeArgs a{st->w_qkv, NQKV, pool(st, l), c.bt, c.ctx, st->w_part_o, st->w_part_ml,
                        st->w_attn, QD, c.T, m.n_heads, m.n_kv_heads, D, st->max_blocks_per_seq,
                        st->max_splits, c.call_splits, c.kv_read_bytes};
-      hipError_t e = attn_decode(a, s, i, nullptr);
-      i->name = "attn_decode";
-      return e;
+      return attn_decode(a, s, i);
     });
   }
   if (r != HS_OK) return r;

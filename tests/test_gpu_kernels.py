@@ -175,6 +175,30 @@ def _paged_case(lens, nh, nkv, d, seed):
     return q, pool, table, ks, vs
 
 
+def test_attn_decode_batch_invariant():
+    """A sequence's output has the same bits alone and inside a ragged
+    16-sequence batch."""
+    torch = G.torch()
+    hs = _hs()
+    lens = [2100] + [int(x) for x in np.random.default_rng(3).integers(900, 2000, 15)]
+    nh, nkv, d = 32, 8, 128
+    q, pool, table, _, _ = _paged_case(lens, nh, nkv, d, 77)
+    dq = G.to_dev_bf16(q)
+    dpool = G.to_dev_bf16(pool.reshape(-1))
+    dtab = torch.from_numpy(table).cuda()
+    dctx = torch.tensor(lens, dtype=torch.int32).cuda()
+    out = torch.zeros((len(lens), nh * d), dtype=torch.bfloat16, device="cuda")
+    hs.hs_k_attn_decode(dq.data_ptr(), nh * d, dpool.data_ptr(), dtab.data_ptr(), dctx.data_ptr(),
+                        out.data_ptr(), nh * d, len(lens), nh, nkv, d, table.shape[1], max(lens),
+                        G.stream_ptr())
+    one = torch.zeros((1, nh * d), dtype=torch.bfloat16, device="cuda")
+    hs.hs_k_attn_decode(dq.data_ptr(), nh * d, dpool.data_ptr(), dtab.data_ptr(), dctx.data_ptr(),
+                        one.data_ptr(), nh * d, 1, nh, nkv, d, table.shape[1], lens[0],
+                        G.stream_ptr())
+    torch.cuda.synchronize()
+    assert np.array_equal(G.from_dev_bf16(one)[0], G.from_dev_bf16(out)[0])
+
+
 @pytest.mark.parametrize("lens,nh,nkv,d", [
     ([1], 4, 4, 64), ([17, 300, 64, 65], 4, 4, 64), ([5, 130, 1100, 64, 2100], 32, 8, 128),
     ([512], 32, 32, 128), ([2, 129, 700], 8, 2, 128), ([1000, 33], 16, 4, 64)])
