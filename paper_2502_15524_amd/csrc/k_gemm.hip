@@ -645,16 +645,18 @@ struct RingCfg {
   bool sk_ok;  // has a stream-K build
 };
 const RingCfg kRing[] = {{"256x256", 256, 256, false}, {"256x128", 256, 128, true},
-                         {"128x128", 128, 128, true},  {"192x256", 192, 256, false}};
+                         {"128x128", 128, 128, true},  {"192x256", 192, 256, false},
+                         {"192x128", 192, 128, false}};
 
 // 256 x 256 and 192 x 256: 2 stages (128 and 112 KiB of LDS), the next
 // stage's loads issued in the first half of the current one's
 // multiplication. 256 x 128: 3 stages, loads spread over the whole step.
-// 128 x 128: 4 stages.
+// 192 x 128 (160 KiB) and 128 x 128: 4 stages.
 hipError_t launch_ring(const RingCfg& c, const GemmArgs& a, int epi, const GemmSched& sc,
                        int grid, hipStream_t s) {
   if (c.bn == 256 && c.bm == 256) return dispatch_ring<256, 256, 2, 2, false>(a, epi, sc, grid, s);
   if (c.bn == 192 && c.bm == 256) return dispatch_ring<192, 256, 2, 2, false>(a, epi, sc, grid, s);
+  if (c.bn == 192 && c.bm == 128) return dispatch_ring<192, 128, 4, 4, false>(a, epi, sc, grid, s);
   if (c.bn == 256 && c.bm == 128)
     return sc.sk ? dispatch_ring<256, 128, 3, 4, true>(a, epi, sc, grid, s)
                  : dispatch_ring<256, 128, 3, 4, false>(a, epi, sc, grid, s);
@@ -761,12 +763,15 @@ hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info) {
       return c.sk_ok && g >= 1 && a.part && a.flags && tiles <= a.flags_n &&
              2 * g * (int64_t)c.bn * c.bm <= a.part_floats;
     };
-    // 192 x 256 covers more CUs than 256 x 256 when one round of tiles
-    // fills the chip (the gate/up projection of a 512-token 7B prompt: 230
-    // instead of 172 tiles, 102 instead of 118 us on MI355X).
+    // The 192-wide tiles cover more CUs when one round of tiles fills the
+    // chip (512-token 7B prompt, MI355X: gate/up 230 tiles of 192 x 256
+    // instead of 172 of 256 x 256, 102 instead of 118 us; QKV 256 tiles of
+    // 192 x 128 instead of 192 of 256 x 128, 54 instead of 67 us); over
+    // several rounds they lose to the 256-wide ones (4096-wide projections of
+    // 8192 tokens: 20% slower), so they only run as a single round.
     const Cand cands[] = {{&kRing[0], false, 4.8}, {&kRing[1], false, 4.05},
                           {&kRing[2], false, 3.05}, {&kRing[2], true, 3.0},
-                          {&kRing[3], false, 4.45}};
+                          {&kRing[3], false, 4.45}, {&kRing[4], false, 3.9}};
     const double sk_fixed_us = 10.0;
     const RingCfg* cfg = nullptr;
     bool sk = false;
@@ -776,6 +781,7 @@ hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info) {
       const long tiles = tiles_of(c);
       double us;
       if (!cands[i].sk) {
+        if (c.bn == 192 && tiles > cus) continue;
         const long rounds = (tiles + cus - 1) / cus;
         us = rounds * (2.0 * kp * c.bn * c.bm) / (cands[i].rate * 1e6);
       } else {
