@@ -586,9 +586,19 @@ def bench_pipeline(wl, args):
         tgt.close()
         ms_imp = statistics.median(imp_ms)
         ms_exp = sum(exp_ms)
+        # reference: a plain device-to-device copy of the same bytes
+        copy_ms = 0.0
+        with torch.cuda.stream(stream):
+            for b, n in blobs:
+                dst_b = torch.empty_like(b)
+                dst_b.copy_(b)
+                ms_c, _ = timed(lambda: dst_b.copy_(b), 5)
+                copy_ms += ms_c
+                del dst_b
         log(f"[bench] KV export {moved / 1e9:.2f} GB in {ms_exp:.2f} ms "
             f"({2 * moved / (ms_exp / 1e3) / 1e9:,.0f} GB/s), import {ms_imp:.2f} ms "
-            f"({2 * moved / (ms_imp / 1e3) / 1e9:,.0f} GB/s)")
+            f"({2 * moved / (ms_imp / 1e3) / 1e9:,.0f} GB/s); a plain device copy of the "
+            f"same blobs {copy_ms:.2f} ms ({2 * moved / (copy_ms / 1e3) / 1e9:,.0f} GB/s)")
         # the merge itself: stage 0 takes over every layer (drain, block
         # copies into its pools, serving range extended), then decodes alone
         ms_merge, _ = timed(lambda: hs.hs_stage_merge(stages[0].h, [st.h for st in stages[1:]],
@@ -597,6 +607,7 @@ def bench_pipeline(wl, args):
         log(f"[bench] merge {ms_merge:.2f} ms; merged-worker decode B={B} {ms_dec_m:.3f} "
             f"ms/step = {B / ms_dec_m * 1e3:,.0f} tok/s")
         res_extra = {"kv_export_ms": round(ms_exp, 3), "kv_import_ms": round(ms_imp, 3),
+                     "device_copy_same_bytes_ms": round(copy_ms, 3),
                      "kv_bytes": moved,
                      "kv_export_GBps": round(2 * moved / (ms_exp / 1e3) / 1e9, 1),
                      "kv_import_GBps": round(2 * moved / (ms_imp / 1e3) / 1e9, 1),
