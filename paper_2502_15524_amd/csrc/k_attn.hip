@@ -20,7 +20,7 @@ namespace hs {
 // query then live in the 4 lanes l, l+16, l+32, l+48. P^T feeds the second
 // MFMA as its B operand with the key order of each 32-key step permuted
 // (lane group g, element e -> key 4g+e for e<4, 16+4g+e-4 otherwise); V^T is
-// read from LDS with the same permutation, so the product is unchanged.
+// stored in LDS in that permuted order, so the product is unchanged.
 
 template <int D, int NW>
 __global__ __launch_bounds__(64 * NW) void attn_prefill_kernel(AttnPrefillArgs a, float scale_log2) {
@@ -28,13 +28,14 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_kernel(AttnPrefillArgs a
   constexpr int QT = 16 * NW;   // queries per workgroup
   constexpr int KB = 64;        // keys per block
   constexpr int LK = D + 8;     // padded K row in LDS
-  constexpr int LV = KB + 2;    // padded V^T row in LDS (33 dwords)
+  constexpr int LVW = KB / 2 + 4;  // V^T row in 32-bit words (key pairs): 16-byte aligned,
+                                   // the 16 rows of a fragment on distinct banks
   constexpr int CPK = D / 8;    // 16-byte chunks per key row
   constexpr int KPP = NT / CPK; // key rows per load pass
   constexpr int PASS = KB / KPP;
   static_assert(KB % KPP == 0 && (KPP % 2) == 0, "load mapping");
   __shared__ __attribute__((aligned(16))) bf16_t sK[KB * LK];
-  __shared__ __attribute__((aligned(16))) uint32_t sVt[D * LV / 2];
+  __shared__ __attribute__((aligned(16))) uint32_t sVt[D * LVW];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int seq = a.tiles[2 * blockIdx.x], q0 = a.tiles[2 * blockIdx.x + 1];
@@ -84,14 +85,18 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_kernel(AttnPrefillArgs a
       st16(&sK[key * LK + lcol], kreg[p]);
       // V^T: keys (2j, 2j+1) sit in lanes L and L ^ CPK; the even-key lane
       // writes columns lcol..+3 and the odd-key lane lcol+4..+7, each as
-      // 4-byte (key pair) words.
+      // 4-byte (key pair) words. Within each 32-key half of a row the pairs
+      // are stored in the order the PV MFMA's lane groups read them (group
+      // g: keys 4g..4g+3 and 16+4g..16+4g+3), so a fragment is one 16-byte
+      // read.
       uint32_t pw[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) pw[e] = __shfl_xor(vreg[p].w[e], CPK, 64);
       // selections by bit mask (all ones for an odd key): with a ternary the
       // compiler turns the pick into a runtime index into scratch memory
       const uint32_t odd = 0u - (uint32_t)(key & 1);
-      const int kp = key >> 1;
+      const int kp = key >> 1, j = kp & 15;
+      const int word = (kp >> 4) * 16 + ((j & 7) >> 1) * 4 + (j >> 3) * 2 + (j & 1);
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
         const uint32_t mine = vreg[p].w[e] ^ ((vreg[p].w[e] ^ vreg[p].w[2 + e]) & odd);
@@ -99,8 +104,8 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_kernel(AttnPrefillArgs a
         const uint32_t ev = mine ^ ((mine ^ other) & odd);   // even key's word
         const uint32_t od = other ^ ((other ^ mine) & odd);  // odd key's word
         const int col = lcol + (key & 1) * 4 + 2 * e;
-        sVt[(col) * (LV / 2) + kp] = (ev & 0xFFFFu) | (od << 16);
-        sVt[(col + 1) * (LV / 2) + kp] = (ev >> 16) | (od & 0xFFFF0000u);
+        sVt[col * LVW + word] = (ev & 0xFFFFu) | (od << 16);
+        sVt[(col + 1) * LVW + word] = (ev >> 16) | (od & 0xFFFF0000u);
       }
     }
     __syncthreads();
@@ -155,15 +160,9 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_kernel(AttnPrefillArgs a
       pb.w[2] = pack2bf(s[2 * st + 1][0], s[2 * st + 1][1]);
       pb.w[3] = pack2bf(s[2 * st + 1][2], s[2 * st + 1][3]);
       const bf16x8_v pf = as_bf16x8(pb);
-      const int k1 = (st * 32 + g * 4) >> 1, k2 = (st * 32 + 16 + g * 4) >> 1;
 #pragma unroll
       for (int dt = 0; dt < D / 16; ++dt) {
-        const uint32_t* row = &sVt[(dt * 16 + fr) * (LV / 2)];
-        pack8 vb;
-        vb.w[0] = row[k1];
-        vb.w[1] = row[k1 + 1];
-        vb.w[2] = row[k2];
-        vb.w[3] = row[k2 + 1];
+        const pack8 vb = ld16(&sVt[(dt * 16 + fr) * LVW + st * 16 + g * 4]);
         o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vb), pf, o[dt], 0, 0, 0);
       }
     }
