@@ -15,9 +15,9 @@
 // Two kernels:
 //  * gemm_ring   - prefill: BN x BM x 64 tiles copied straight into an LDS ring
 //                  of NS stages, 4 waves, 16x16x32 bf16 MFMA, XCD-aware order.
-//  * gemm_skinny - decode (M <= 64 tokens): HBM-bound weight streaming, 4
-//                  waves split K inside a workgroup, reduced through LDS in a
-//                  fixed order (deterministic).
+//  * gemm_skinny - decode (M <= 64 tokens): HBM-bound weight streaming, 4 or
+//                  8 waves split K inside a workgroup, reduced through LDS in
+//                  a fixed order (deterministic).
 #include "hs_device.h"
 #include "hs_kernels.h"
 
@@ -426,7 +426,7 @@ void gemm_ring(GemmArgs a, GemmSched sc) {
 
 // ------------------------------------------------------------ skinny (decode)
 //
-// A workgroup owns 16 * NF weight rows and all M <= 64 tokens; its 4 waves
+// A workgroup owns 16 * NF weight rows and all M <= 64 tokens; its WV waves
 // split the 64-column slabs of K. For one slab, the rows' two (or four) 1 KiB
 // blocks are adjacent, so a wave reads 2 KiB per 16 rows contiguously; lane
 // (row fr, group g) takes chunk 4 ks + g of its row for the ks-th 32-k MFMA.
