@@ -718,8 +718,12 @@ hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info) {
     // depend on how many tokens share the call.
     // HS_SKINNY_CFG="<NF>,<U>,<WV>" forces a choice (tuning only).
     static const char* force = getenv("HS_SKINNY_CFG");
-    int nf = 1, u = 4, wv = 4;  // LM head
-    if (epi == EPI_SWIGLU) {
+    int nf = 1, u = 4, wv = 4;
+    if (epi == EPI_F32) {
+      // LM head: above 4 tokens, four row tiles per workgroup (128256 wide:
+      // 261 -> 217 us at 16 tokens)
+      if (a.M > 4) nf = 4, u = 1;
+    } else if (epi == EPI_SWIGLU) {
       nf = (a.M > 8 && a.N >= 16384) ? 4 : 2, u = 1;
     } else if (epi == EPI_RESID) {
       if (a.M > 4 && a.N / 16 > device_cus()) nf = 2, u = 1, wv = 8;
