@@ -15,9 +15,9 @@
 // Two kernels:
 //  * gemm_ring   - prefill: BN x BM x 64 tiles copied straight into an LDS ring
 //                  of NS stages, 4 waves, 16x16x32 bf16 MFMA, XCD-aware order.
-//  * gemm_skinny - decode (M <= 64 tokens): HBM-bound weight streaming, 4 or
-//                  8 waves split K inside a workgroup, reduced through LDS in
-//                  a fixed order (deterministic).
+//  * gemm_skinny - decode (M <= 64 tokens): HBM-bound weight streaming, 2,
+//                  4 or 8 waves split K inside a workgroup, reduced through
+//                  LDS in a fixed order (deterministic).
 #include "hs_device.h"
 #include "hs_kernels.h"
 
@@ -427,9 +427,29 @@ void gemm_ring(GemmArgs a, GemmSched sc) {
 // ------------------------------------------------------------ skinny (decode)
 //
 // A workgroup owns 16 * NF weight rows and all M <= 64 tokens; its WV waves
-// split the 64-column slabs of K. For one slab, the rows' two (or four) 1 KiB
-// blocks are adjacent, so a wave reads 2 KiB per 16 rows contiguously; lane
-// (row fr, group g) takes chunk 4 ks + g of its row for the ks-th 32-k MFMA.
+// split the 64-column slabs of K. For one slab, the 2 NF row blocks of the
+// workgroup are adjacent 1 KiB blocks. Each is read by one wave-wide 16-byte
+// load with lane L taking bytes [16 L, 16 L + 16) (a whole block per
+// instruction, non-temporal: the weights are streamed once per call), then
+// stored unchanged into the wave's own LDS buffer and read back in the MFMA
+// fragment order: lane (row fr, group g) takes chunk 4 ks + g of its row for
+// the ks-th 32-k MFMA. The buffer keeps the block's XOR-swizzled chunk order,
+// so the fragment reads are free of bank conflicts. (Loading the fragments
+// straight from global memory makes every instruction touch half of each of
+// 16 rows; the whole-block loads stream 10-30% faster on MI355X.) The loads
+// of the next slab group are issued before the current one is multiplied.
+
+typedef uint32_t u32x4_v __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ pack8 ld16_nt(const void* p) {
+  const u32x4_v v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_v*>(p));
+  pack8 r;
+  r.w[0] = v[0];
+  r.w[1] = v[1];
+  r.w[2] = v[2];
+  r.w[3] = v[3];
+  return r;
+}
 
 // With NORM, X is the un-normalised residual stream and the GEMM applies the
 // RMSNorm of its rows itself: each loaded activation chunk is multiplied by
@@ -448,22 +468,22 @@ __global__ __launch_bounds__(64 * WV) void gemm_skinny(GemmArgs a) {
   const int sb = wave * sq, se = min(nslab, sb + sq);
   const int fr = lane & 15, g = lane >> 4;
   const int64_t slab_bytes = (int64_t)(a.N / 8) * 1024;
-
-  const char* wrow[NF];
+  // instruction (f, h) of a slab reads row block n0 / 8 + 2 f + h (N % 16 == 0,
+  // so a 16-row tile is either wholly inside the matrix or wholly outside)
+  const char* wbase = reinterpret_cast<const char*>(a.W) + (int64_t)(n0 / 8) * 1024 + lane * 16;
   bool wok[NF];
 #pragma unroll
-  for (int f = 0; f < NF; ++f) {
-    const int n = n0 + 16 * f + fr;
-    wok[f] = n < a.N;
-    wrow[f] = reinterpret_cast<const char*>(a.W) + (int64_t)(n / 8) * 1024 + (n % 8) * 128;
-  }
+  for (int f = 0; f < NF; ++f) wok[f] = n0 + 16 * f < a.N;
   const int r8 = fr % 8;
+  // 16-byte position of lane (fr, g)'s row inside the 2 KiB image of a 16-row tile
+  const int fpos = (fr / 8) * 64 + r8 * 8;
   const bf16_t* xrow[MCH];
 #pragma unroll
   for (int c = 0; c < MCH; ++c) {
     const int m = 16 * c + fr;
     xrow[c] = (m < a.M) ? a.X + (int64_t)m * a.ldx : nullptr;
   }
+  __shared__ pack8 wlds[WV][U][NF * 128];
 
   f32x4_v acc[NF][MCH];
   float ssq[MCH];
@@ -474,8 +494,32 @@ __global__ __launch_bounds__(64 * WV) void gemm_skinny(GemmArgs a) {
 #pragma unroll
   for (int c = 0; c < MCH; ++c) ssq[c] = 0.f;
 
+  pack8 wv[U][NF][2];
+  auto load_w = [&](int s0) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int sl = s0 + u;
+      const bool ok = sl < se;
+#pragma unroll
+      for (int f = 0; f < NF; ++f)
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+          wv[u][f][h] = (ok && wok[f]) ? ld16_nt(wbase + sl * slab_bytes + (2 * f + h) * 1024)
+                                       : zero8();
+    }
+  };
+  if (sb < se) load_w(sb);
   for (int s0 = sb; s0 < se; s0 += U) {
-    pack8 wv[NF][U][2], xv[MCH][U][2], gv[U][2];
+    // this wave's buffer: the previous group's fragment reads were issued
+    // before these stores, and one wave's LDS operations run in order
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int f = 0; f < NF; ++f)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) wlds[wave][u][(2 * f + h) * 64 + lane] = wv[u][f][h];
+    if (s0 + U < se) load_w(s0 + U);
+    pack8 xv[MCH][U][2], gv[U][2];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int sl = s0 + u;
@@ -483,11 +527,6 @@ __global__ __launch_bounds__(64 * WV) void gemm_skinny(GemmArgs a) {
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
         const int chunk = ks * 4 + g;
-#pragma unroll
-        for (int f = 0; f < NF; ++f)
-          wv[f][u][ks] = (ok && wok[f])
-                             ? ld16(wrow[f] + sl * slab_bytes + ((chunk ^ r8) * 16))
-                             : zero8();
 #pragma unroll
         for (int c = 0; c < MCH; ++c)
           xv[c][u][ks] = (ok && xrow[c]) ? ld16(xrow[c] + sl * 64 + chunk * 8) : zero8();
@@ -510,16 +549,20 @@ __global__ __launch_bounds__(64 * WV) void gemm_skinny(GemmArgs a) {
             }
           }
     }
+    asm volatile("" ::: "memory");  // keep the fragment reads after the stores
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-        for (int f = 0; f < NF; ++f)
+        for (int f = 0; f < NF; ++f) {
+          const pack8 w = wlds[wave][u][f * 128 + fpos + ((ks * 4 + g) ^ r8)];
 #pragma unroll
           for (int c = 0; c < MCH; ++c)
             acc[f][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                as_bf16x8(wv[f][u][ks]), as_bf16x8(xv[c][u][ks]), acc[f][c], 0, 0, 0);
+                as_bf16x8(w), as_bf16x8(xv[c][u][ks]), acc[f][c], 0, 0, 0);
+        }
+    asm volatile("" ::: "memory");  // and the next stores after these reads
   }
 
   __shared__ f32x4_v red[WV - 1][NF][MCH][64];
@@ -617,7 +660,8 @@ hipError_t dispatch_epi_skinny(const GemmArgs& a, int epi, hipStream_t s) {
 // The skinny variants built for one 16-token chunk, as (rows per workgroup /
 // 16, slabs unrolled per wave, waves per workgroup): the ones the selection
 // in gemm() takes.
-#define HS_SKINNY_MCH1(X) X(1, 4, 4) X(1, 1, 8) X(1, 2, 8) X(2, 1, 4) X(2, 1, 8) X(4, 1, 4)
+#define HS_SKINNY_MCH1(X) \
+  X(1, 1, 8) X(1, 2, 8) X(2, 1, 8) X(2, 1, 4) X(4, 1, 4) X(2, 1, 2) X(4, 1, 2) X(8, 1, 2)
 
 hipError_t dispatch_skinny1(const GemmArgs& a, int epi, int nf, int u, int wv, hipStream_t s) {
 #define HS_SKINNY_CASE(NF_, U_, WV_) \
@@ -706,30 +750,33 @@ hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info) {
   hipError_t e;
   if (a.M <= 64) {
     const int mch = (a.M + 15) / 16;
-    // Rows per workgroup (16 NF), 64-k slabs unrolled per wave (U) and waves
-    // per workgroup (WV) for one token chunk, from a sweep on MI355X over the
-    // decode projections of 7B, 8B and 13B models at 1, 8 and 16 tokens:
+    // Rows per workgroup (16 NF), 64-k slabs per load group (U) and waves per
+    // workgroup (WV) for one token chunk, from a sweep on MI355X over the
+    // decode projections of 7B, 8B and 13B models at 1, 4, 8 and 16 tokens:
     // narrow outputs (o, down, QKV up to 8192 wide) fill the chip with eight
-    // waves per workgroup, wide ones (QKV, gate/up) with four; above 8 tokens
-    // wide gate/up reads more rows per activation fetch, and so do o/down
-    // above 4 tokens when one row tile per CU does not cover them (5120
-    // wide: 40.3 instead of 55.0 us at 16 tokens). WV depends on the
-    // shape only, never on M, so that a token's result (its k order) does not
-    // depend on how many tokens share the call.
+    // waves per workgroup, wide QKV and gate/up with four; gate/up takes four
+    // row tiles per workgroup once that still gives 1.5 workgroups per CU
+    // (8B, 13B: 38 and 45 instead of 43 and 52 us); o/down wider than one
+    // row tile per CU take one slab per group up to 4 tokens and two row
+    // tiles above; the LM head runs two waves over as many row tiles as keep
+    // about a thousand workgroups (128256 wide: 155 instead of 162-169 us).
+    // WV depends on the shape only, never on M, so that a token's result (its
+    // k order) does not depend on how many tokens share the call.
     // HS_SKINNY_CFG="<NF>,<U>,<WV>" forces a choice (tuning only).
     static const char* force = getenv("HS_SKINNY_CFG");
-    int nf = 1, u = 4, wv = 4;
+    const int cus = device_cus();
+    int nf = 1, u = 1, wv = 4;
     if (epi == EPI_F32) {
-      // LM head: above 4 tokens, four row tiles per workgroup (128256 wide:
-      // 261 -> 217 us at 16 tokens)
-      if (a.M > 4) nf = 4, u = 1;
+      nf = 2, wv = 2;
+      while (nf < 8 && a.N / (16 * nf) > 1100) nf *= 2;
     } else if (epi == EPI_SWIGLU) {
-      nf = (a.M > 8 && a.N >= 16384) ? 4 : 2, u = 1;
+      nf = (a.N / 64 >= cus + cus / 2) ? 4 : 2;
     } else if (epi == EPI_RESID) {
-      if (a.M > 4 && a.N / 16 > device_cus()) nf = 2, u = 1, wv = 8;
-      else nf = 1, u = a.M <= 8 ? 2 : 1, wv = 8;
+      wv = 8;
+      if (a.N / 16 > cus) nf = a.M > 4 ? 2 : 1;
+      else u = a.M <= 8 ? 2 : 1;
     } else if (epi == EPI_STORE) {
-      nf = 2, u = 1, wv = a.N <= 8192 ? 8 : 4;
+      nf = 2, wv = a.N <= 8192 ? 8 : 4;
     }
     if (force && *force) sscanf(force, "%d,%d,%d", &nf, &u, &wv);
     if (epi == EPI_SWIGLU && (nf % 2)) nf = 2;

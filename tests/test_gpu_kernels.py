@@ -21,7 +21,9 @@ GEMM_SHAPES = [(1, 256, 256), (7, 768, 256), (16, 1376, 256), (33, 512, 688),
                (777, 1376, 688), (1024, 4096, 4096),
                (12, 16384, 256), (16, 6144, 512),   # wide 9-16-token decode variants
                (3, 2048, 11008), (14, 1024, 5120),  # eight-wave splits of a long k
-               (512, 22016, 256), (512, 12288, 256)]  # one round of 192 x 256, 192 x 128 tiles
+               (512, 22016, 256), (512, 12288, 256),  # one round of 192 x 256, 192 x 128 tiles
+               (4, 73728, 256), (3, 36864, 320),    # LM-head-wide: 8 and 4 row tiles, 2 waves
+               (9, 5120, 256), (5, 24576, 192)]     # o/down wider than the CUs; 4-tile gate/up
 
 
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
