@@ -1290,17 +1290,24 @@ extern "C" hs_status hs_kv_import(hs_stage* st, const void* src, uint64_t bytes,
   hipStream_t s = pick(st, stream);
   hs_status r = begin_call(st, s);
   if (r != HS_OK) return r;
-  std::vector<uint8_t> head(kBlobHeader);
-  HIPTRY(hipMemcpyAsync(head.data(), src, kBlobHeader, hipMemcpyDeviceToHost, s));
+  // one read covers the header and up to 256 sequence records; a blob with
+  // more sequences takes a second read for the rest
+  const uint64_t first = std::min<uint64_t>(bytes, kBlobHeader + kBlobRecord * 256);
+  std::vector<uint8_t> head(first);
+  HIPTRY(hipMemcpyAsync(head.data(), src, first, hipMemcpyDeviceToHost, s));
   HIPTRY(hipStreamSynchronize(s));
   int32_t ns = 0;
   memcpy(&ns, head.data() + 32, 4);
   if (ns < 0 || kBlobHeader + kBlobRecord * (uint64_t)ns > bytes)
     return fail(HS_EINVAL, "blob sequence count does not fit its length");
-  head.resize(kBlobHeader + kBlobRecord * (uint64_t)ns);
-  if (ns > 0) {
-    HIPTRY(hipMemcpyAsync(head.data(), src, head.size(), hipMemcpyDeviceToHost, s));
+  const uint64_t need = kBlobHeader + kBlobRecord * (uint64_t)ns;
+  if (need > first) {
+    head.resize(need);
+    HIPTRY(hipMemcpyAsync(head.data() + first, static_cast<const uint8_t*>(src) + first,
+                          need - first, hipMemcpyDeviceToHost, s));
     HIPTRY(hipStreamSynchronize(s));
+  } else {
+    head.resize(need);
   }
   BlobHeader h;
   std::vector<BlobRecord> recs;

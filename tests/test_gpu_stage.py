@@ -204,6 +204,31 @@ def test_kv_export_import_roundtrip_bitwise(env):
     assert b1 == b2
 
 
+def test_kv_roundtrip_many_sequences_bitwise(env):
+    """A blob with more sequence records than the importer reads with the
+    header in its first copy (300 sequences of 1-40 tokens)."""
+    torch = G.torch()
+    hs = env["hs"]
+    n = 300
+    lens = [int(x) for x in np.random.default_rng(300).integers(1, 41, n)]
+    ids = list(range(1000, 1000 + n))
+    toks = gen.tokens(CFG.vocab, sum(lens), 31)
+    src = make(env, 0, 1, max_seqs=n, max_ctx=64, max_batch_tokens=sum(lens))
+    x = torch.from_numpy(np.asarray(toks, np.int32)).cuda()
+    out = torch.zeros((sum(lens), CFG.hidden), dtype=torch.bfloat16, device="cuda")
+    src.prefill(ids, lens, x.data_ptr(), out.data_ptr(), 0, G.stream_ptr())
+    order = ids[::-1]
+    blob = _export(src, order)
+    b1 = blob.cpu().numpy().tobytes()
+    hdr, _ = kvblob.parse(b1)
+    assert len(hdr["records"]) == n
+    dst = make(env, 0, 1, max_seqs=n, max_ctx=64, max_batch_tokens=sum(lens))
+    hs.hs_kv_import(dst.h, blob.data_ptr(), blob.numel(), G.stream_ptr())
+    for i, ln in zip(ids, lens):
+        assert hs.hs_seq_tokens(dst.h, i) == ln
+    assert _export(dst, order).cpu().numpy().tobytes() == b1
+
+
 def test_import_then_continue_decoding_bitwise(env):
     """Checkpoint/resume: a stage rebuilt from a blob decodes exactly like
     the original."""
