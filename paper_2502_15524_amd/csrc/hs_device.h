@@ -35,6 +35,18 @@ __device__ __forceinline__ float hi_bf(uint32_t w) { return __uint_as_float(w & 
 __device__ __forceinline__ pack8 ld16(const void* p) {
   return *reinterpret_cast<const pack8*>(p);
 }
+// 16 bytes read once per call (weights, cached keys and values): a
+// non-temporal load
+__device__ __forceinline__ pack8 ld16_nt(const void* p) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  pack8 r;
+  r.w[0] = v[0];
+  r.w[1] = v[1];
+  r.w[2] = v[2];
+  r.w[3] = v[3];
+  return r;
+}
 __device__ __forceinline__ void st16(void* p, const pack8& v) {
   *reinterpret_cast<pack8*>(p) = v;
 }

@@ -331,7 +331,8 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a
   const int h0 = kh * G;
   const int64_t kv_stride = (int64_t)a.n_kv_heads * 16 * D;  // K block -> V block
 
-  // all key and value loads of the split go out first
+  // all key and value loads of the split go out first (non-temporal: each
+  // cached byte is read once per step)
   pack8 kv[PASSES], vv[PASSES];
 #pragma unroll
   for (int p = 0; p < PASSES; ++p) {
@@ -342,8 +343,8 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a
       const int ph = TPP == 16 ? phys[p] : ((tl >> 4) ? phys[2 * p + 1] : phys[2 * p]);
       const bf16_t* kp = a.pool + ((int64_t)ph * 2 * a.n_kv_heads + kh) * 16 * D +
                          (tok & 15) * D + c * 8;
-      kv[p] = ld16(kp);
-      vv[p] = ld16(kp + kv_stride);
+      kv[p] = ld16_nt(kp);
+      vv[p] = ld16_nt(kp + kv_stride);
     }
   }
   float q[G][8];

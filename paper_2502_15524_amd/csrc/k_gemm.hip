@@ -439,18 +439,6 @@ void gemm_ring(GemmArgs a, GemmSched sc) {
 // 16 rows; the whole-block loads stream 10-30% faster on MI355X.) The loads
 // of the next slab group are issued before the current one is multiplied.
 
-typedef uint32_t u32x4_v __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ pack8 ld16_nt(const void* p) {
-  const u32x4_v v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_v*>(p));
-  pack8 r;
-  r.w[0] = v[0];
-  r.w[1] = v[1];
-  r.w[2] = v[2];
-  r.w[3] = v[3];
-  return r;
-}
-
 // With NORM, X is the un-normalised residual stream and the GEMM applies the
 // RMSNorm of its rows itself: each loaded activation chunk is multiplied by
 // the norm gain (and rounded to bf16 like a stored activation), the squares
