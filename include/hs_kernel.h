@@ -76,6 +76,27 @@ hs_status hs_k_attn_decode(const void* q, int64_t ldq, const void* pool,
                            int32_t head_dim, int32_t max_blocks, int32_t max_ctx,
                            void* stream);
 
+/* The same attention with the decode step's RoPE and cache append folded in
+ * (LLM inference: the new token's key and value join the cache and every
+ * later step reuses them). qkv: bf16 [B][ldqkv], the QKV projection of each
+ * sequence's new token before RoPE (query heads, then key heads, then value
+ * heads, head_dim columns each); the new token sits at position ctx - 1 of
+ * its sequence and is NOT read from the pool: the call rotates the queries
+ * and the new key by the rotate-half RoPE at that position (float32
+ * arithmetic, bf16 rounding), attends over the cached tokens plus the new
+ * one, and writes the rotated key and the value into the token's slot of
+ * pool (block block_table[b][(ctx - 1) / 16], offset (ctx - 1) % 16), which
+ * the caller must have allocated. cos_t, sin_t: device float32
+ * [max_pos][head_dim / 2], cos and sin of pos * base^(-2 i / head_dim);
+ * max_ctx <= max_pos. Other arguments, workspace and errors as for
+ * hs_k_attn_decode. */
+hs_status hs_k_attn_decode_rope(const void* qkv, int64_t ldqkv, void* pool,
+                                const int32_t* block_table, const int32_t* ctx,
+                                const float* cos_t, const float* sin_t, int32_t max_pos,
+                                void* out, int64_t ldo, int32_t B, int32_t n_heads,
+                                int32_t n_kv_heads, int32_t head_dim, int32_t max_blocks,
+                                int32_t max_ctx, void* stream);
+
 /* RMSNorm of `rows` rows of width `hidden`: out = x / sqrt(mean(x^2) + eps) * g,
  * bf16 in and out, float32 arithmetic. */
 hs_status hs_k_rmsnorm(const void* x, const void* g, void* out, int32_t rows, int32_t hidden,

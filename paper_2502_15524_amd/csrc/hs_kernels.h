@@ -88,6 +88,16 @@ struct AttnDecodeArgs {
   bf16_t* out; int64_t ldo;       // [B][n_heads * D]
   int B, n_heads, n_kv_heads, D, max_blocks, max_splits, call_splits;
   double kv_bytes;                // bytes of K/V read, for reporting
+  // Fused RoPE and cache append (decode steps): when pool_w is set, q points
+  // at the rows of the QKV projection before RoPE ([B][ldq]: query heads,
+  // then key heads, then value heads), position ctx - 1 of each sequence is
+  // the new token, whose key and value are read from those rows instead of
+  // the pool; the kernel rotates the queries and the new key (the rotation
+  // and bf16 rounding of rope_kv) and writes the new key and value into the
+  // token's slot of pool_w (the same pool as `pool`).
+  bf16_t* pool_w = nullptr;
+  const float* cos_t = nullptr; const float* sin_t = nullptr;  // [max_pos][D/2]
+  int max_pos = 0;
 };
 hipError_t attn_decode(const AttnDecodeArgs& a, hipStream_t s, LaunchInfo* info);
 

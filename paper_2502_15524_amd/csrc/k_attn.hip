@@ -302,8 +302,35 @@ __device__ __forceinline__ float merge_splits(__amdgpu_buffer_rsrc_t ro, __amdgp
   return O / L;
 }
 
-template <int D, int G>
+// Rotate-half RoPE of one 16-byte chunk (8 consecutive elements of a head)
+// whose partner chunk (the elements D/2 away) sits in lane ^ (LPT / 2): the
+// first half's lanes get x1 c - x2 s, the second half's x2 c + x1 s, in
+// float32, rounded to bf16 (the arithmetic and rounding of rope_kv). Every
+// lane of the wave must call it.
+template <int LPT>
+__device__ __forceinline__ pack8 rope_chunk(const pack8& x, bool first, const float (&cs)[8],
+                                            const float (&sn)[8]) {
+  pack8 y;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const uint32_t pw = __shfl_xor(x.w[e], LPT / 2, 64);
+    const float o0 = lo_bf(x.w[e]), o1 = hi_bf(x.w[e]), p0 = lo_bf(pw), p1 = hi_bf(pw);
+    float y0, y1;
+    if (first) {
+      y0 = o0 * cs[2 * e] - p0 * sn[2 * e];
+      y1 = o1 * cs[2 * e + 1] - p1 * sn[2 * e + 1];
+    } else {
+      y0 = o0 * cs[2 * e] + p0 * sn[2 * e];
+      y1 = o1 * cs[2 * e + 1] + p1 * sn[2 * e + 1];
+    }
+    y.w[e] = pack2bf(y0, y1);
+  }
+  return y;
+}
+
+template <int D, int G, bool ROPE>
 __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a, float scale_log2) {
+
   constexpr int LPT = D / 8;        // lanes per token
   constexpr int TPP = 256 / LPT;    // tokens per pass
   constexpr int PASSES = kDecodeSplit / TPP;
@@ -331,6 +358,12 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a
   const int h0 = kh * G;
   const int64_t kv_stride = (int64_t)a.n_kv_heads * 16 * D;  // K block -> V block
 
+  // the new token (fused RoPE) sits at offset t_new of this split when that
+  // is below the split length
+  const int t_new = ctx - 1 - t_begin;  // >= 0; uniform
+  const bool has_new = ROPE && t_new < kDecodeSplit;
+  const bf16_t* qrow = a.q + (int64_t)b * a.ldq;
+
   // all key and value loads of the split go out first (non-temporal: each
   // cached byte is read once per step)
   pack8 kv[PASSES], vv[PASSES];
@@ -343,18 +376,62 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a
       const int ph = TPP == 16 ? phys[p] : ((tl >> 4) ? phys[2 * p + 1] : phys[2 * p]);
       const bf16_t* kp = a.pool + ((int64_t)ph * 2 * a.n_kv_heads + kh) * 16 * D +
                          (tok & 15) * D + c * 8;
+      int64_t vo = kv_stride;
+      if (ROPE && tok == ctx - 1) {  // not in the pool yet: the projection's rows
+        kp = qrow + (int64_t)(a.n_heads + kh) * D + c * 8;
+        vo = (int64_t)a.n_kv_heads * D;
+      }
       kv[p] = ld16_nt(kp);
-      vv[p] = ld16_nt(kp + kv_stride);
+      vv[p] = ld16_nt(kp + vo);
+    }
+  }
+  float cs[8], sn[8];
+  const bool first = c < LPT / 2;
+  if constexpr (ROPE) {
+    const int j = (c % (LPT / 2)) * 8;
+    const float* ct = a.cos_t + (int64_t)(ctx - 1) * (D / 2) + j;
+    const float* st = a.sin_t + (int64_t)(ctx - 1) * (D / 2) + j;
+#pragma unroll
+    for (int e = 0; e < 8; e += 4) {
+      const float4 cv = *reinterpret_cast<const float4*>(ct + e);
+      const float4 sv = *reinterpret_cast<const float4*>(st + e);
+      cs[e] = cv.x;
+      cs[e + 1] = cv.y;
+      cs[e + 2] = cv.z;
+      cs[e + 3] = cv.w;
+      sn[e] = sv.x;
+      sn[e + 1] = sv.y;
+      sn[e + 2] = sv.z;
+      sn[e + 3] = sv.w;
     }
   }
   float q[G][8];
 #pragma unroll
   for (int gg = 0; gg < G; ++gg) {
-    const pack8 v = ld16(a.q + (int64_t)b * a.ldq + (h0 + gg) * D + c * 8);
+    pack8 v = ld16(qrow + (h0 + gg) * D + c * 8);
+    if constexpr (ROPE) v = rope_chunk<LPT>(v, first, cs, sn);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       q[gg][2 * e] = lo_bf(v.w[e]);
       q[gg][2 * e + 1] = hi_bf(v.w[e]);
+    }
+  }
+  if (has_new) {
+    // rotate the new key (the whole wave takes part), use it for the scores
+    // and append key and value to the cache
+#pragma unroll
+    for (int p = 0; p < PASSES; ++p) {
+      if (p != t_new / TPP) continue;
+      const pack8 kr = rope_chunk<LPT>(kv[p], first, cs, sn);
+      if (tl == t_new % TPP) {
+        kv[p] = kr;
+        const int blk = t_new / 16;
+        const int ph = blk == 0 ? phys[0] : blk == 1 ? phys[1] : blk == 2 ? phys[2] : phys[3];
+        bf16_t* kd = a.pool_w + ((int64_t)ph * 2 * a.n_kv_heads + kh) * 16 * D +
+                     ((ctx - 1) & 15) * D + c * 8;
+        st16(kd, kr);
+        st16(kd + kv_stride, vv[p]);
+      }
     }
   }
   const int wave = tid >> 6;
@@ -476,7 +553,10 @@ namespace {
 template <int D, int G>
 void launch_split(const AttnDecodeArgs& a, float sl, hipStream_t s) {
   dim3 grid(a.call_splits, a.n_kv_heads, a.B);
-  hipLaunchKernelGGL((attn_decode_split_kernel<D, G>), grid, dim3(256), 0, s, a, sl);
+  if (a.pool_w)
+    hipLaunchKernelGGL((attn_decode_split_kernel<D, G, true>), grid, dim3(256), 0, s, a, sl);
+  else
+    hipLaunchKernelGGL((attn_decode_split_kernel<D, G, false>), grid, dim3(256), 0, s, a, sl);
 }
 template <int D>
 hipError_t launch_split_g(const AttnDecodeArgs& a, int G, float sl, hipStream_t s) {
@@ -494,6 +574,8 @@ hipError_t attn_decode(const AttnDecodeArgs& a, hipStream_t s, LaunchInfo* info)
   if (a.B <= 0) return hipSuccess;
   if ((a.D != 64 && a.D != 128) || a.n_kv_heads <= 0 || a.n_heads % a.n_kv_heads) return hipErrorInvalidValue;
   if (a.call_splits <= 0 || a.call_splits > a.max_splits || (a.ldq % 8)) return hipErrorInvalidValue;
+  if (a.pool_w && (!a.cos_t || !a.sin_t || a.max_pos <= 0 || a.pool_w != a.pool))
+    return hipErrorInvalidValue;
   // byte offsets of one (query head, sequence)'s partials fit 32 bits
   if ((int64_t)a.max_splits * a.D * 4 >= (1ll << 31)) return hipErrorInvalidValue;
   const int G = a.n_heads / a.n_kv_heads;

@@ -142,40 +142,74 @@ struct DecodeWs {
 };
 }  // namespace
 
+namespace {
+hs_status attn_decode_entry(const void* q, int64_t ldq, const void* pool, bf16_t* pool_w,
+                            const int32_t* block_table, const int32_t* ctx, const float* cos_t,
+                            const float* sin_t, int32_t max_pos, void* out, int64_t ldo,
+                            int32_t B, int32_t n_heads, int32_t n_kv_heads, int32_t head_dim,
+                            int32_t max_blocks, int32_t max_ctx, void* stream) {
+  if (!q || !pool || !block_table || !ctx || !out || B < 1 || max_ctx < 1)
+    return fail(HS_EINVAL, "bad arguments");
+  if (n_kv_heads < 1 || n_heads % n_kv_heads) return fail(HS_EINVAL, "bad head counts");
+  if (max_blocks < (max_ctx + 15) / 16) return fail(HS_EINVAL, "block table too narrow");
+  if (pool_w && (!cos_t || !sin_t || max_pos < max_ctx))
+    return fail(HS_EINVAL, "RoPE tables missing or shorter than max_ctx");
+  static DecodeWs ws[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+    return fail(HS_EHIP, "hipGetDevice failed");
+  const int max_splits = (max_ctx + kDecodeSplit - 1) / kDecodeSplit;
+  const int64_t need = (int64_t)B * n_heads * max_splits * (head_dim + 2);
+  DecodeWs& w = ws[dev];
+  if (w.floats < need) {
+    if (w.buf) {
+      (void)hipDeviceSynchronize();
+      (void)hipFree(w.buf);
+      w.buf = nullptr;
+      w.floats = 0;
+    }
+    if (hipMalloc(reinterpret_cast<void**>(&w.buf), need * sizeof(float)) != hipSuccess)
+      return fail(HS_ENOMEM, "attention workspace");
+    w.floats = need;
+  }
+  AttnDecodeArgs a{static_cast<const bf16_t*>(q), ldq, static_cast<const bf16_t*>(pool),
+                   block_table, ctx, w.buf, w.buf + (int64_t)B * n_heads * max_splits * head_dim,
+                   static_cast<bf16_t*>(out), ldo, B, n_heads, n_kv_heads, head_dim, max_blocks,
+                   max_splits, max_splits, 0.0};
+  a.pool_w = pool_w;
+  a.cos_t = cos_t;
+  a.sin_t = sin_t;
+  a.max_pos = max_pos;
+  return launched(attn_decode(a, static_cast<hipStream_t>(stream), nullptr), "attn_decode");
+}
+}  // namespace
+
 extern "C" hs_status hs_k_attn_decode(const void* q, int64_t ldq, const void* pool,
                                       const int32_t* block_table, const int32_t* ctx, void* out,
                                       int64_t ldo, int32_t B, int32_t n_heads, int32_t n_kv_heads,
                                       int32_t head_dim, int32_t max_blocks, int32_t max_ctx,
                                       void* stream) {
   try {
-    if (!q || !pool || !block_table || !ctx || !out || B < 1 || max_ctx < 1)
-      return fail(HS_EINVAL, "bad arguments");
-    if (n_kv_heads < 1 || n_heads % n_kv_heads) return fail(HS_EINVAL, "bad head counts");
-    if (max_blocks < (max_ctx + 15) / 16) return fail(HS_EINVAL, "block table too narrow");
-    static DecodeWs ws[64];
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
-      return fail(HS_EHIP, "hipGetDevice failed");
-    const int max_splits = (max_ctx + kDecodeSplit - 1) / kDecodeSplit;
-    const int64_t need = (int64_t)B * n_heads * max_splits * (head_dim + 2);
-    DecodeWs& w = ws[dev];
-    if (w.floats < need) {
-      if (w.buf) {
-        (void)hipDeviceSynchronize();
-        (void)hipFree(w.buf);
-        w.buf = nullptr;
-        w.floats = 0;
-      }
-      if (hipMalloc(reinterpret_cast<void**>(&w.buf), need * sizeof(float)) != hipSuccess)
-        return fail(HS_ENOMEM, "attention workspace");
-      w.floats = need;
-    }
-    AttnDecodeArgs a{static_cast<const bf16_t*>(q), ldq, static_cast<const bf16_t*>(pool),
-                     block_table, ctx, w.buf, w.buf + (int64_t)B * n_heads * max_splits * head_dim,
-                     static_cast<bf16_t*>(out), ldo, B, n_heads, n_kv_heads, head_dim, max_blocks,
-                     max_splits, max_splits, 0.0};
-    return launched(attn_decode(a, static_cast<hipStream_t>(stream), nullptr),
-                    "attn_decode");
+    return attn_decode_entry(q, ldq, pool, nullptr, block_table, ctx, nullptr, nullptr, 0, out,
+                             ldo, B, n_heads, n_kv_heads, head_dim, max_blocks, max_ctx, stream);
+  } catch (...) {
+    return fail(HS_EINVAL, "unexpected internal error");
+  }
+}
+
+extern "C" hs_status hs_k_attn_decode_rope(const void* qkv, int64_t ldqkv, void* pool,
+                                           const int32_t* block_table, const int32_t* ctx,
+                                           const float* cos_t, const float* sin_t,
+                                           int32_t max_pos, void* out, int64_t ldo, int32_t B,
+                                           int32_t n_heads, int32_t n_kv_heads, int32_t head_dim,
+                                           int32_t max_blocks, int32_t max_ctx, void* stream) {
+  try {
+    if (!pool) return fail(HS_EINVAL, "bad arguments");
+    if (ldqkv < (int64_t)(n_heads + 2 * n_kv_heads) * head_dim)
+      return fail(HS_EINVAL, "qkv rows narrower than the query, key and value heads");
+    return attn_decode_entry(qkv, ldqkv, pool, static_cast<bf16_t*>(pool), block_table, ctx,
+                             cos_t, sin_t, max_pos, out, ldo, B, n_heads, n_kv_heads, head_dim,
+                             max_blocks, max_ctx, stream);
   } catch (...) {
     return fail(HS_EINVAL, "unexpected internal error");
   }

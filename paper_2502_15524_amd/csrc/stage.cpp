@@ -414,12 +414,15 @@ hs_status layer_forward(hs_stage* st, int l, bf16_t* x, const LayerCall& c, hipS
     return gemm(g, EPI_STORE, s, i);
   });
   if (r != HS_OK) return r;
-  r = run(st, s, "rope_kv", [&](LaunchInfo* i) {
-    RopeKvArgs a{st->w_qkv, NQKV, c.pos, c.slot, st->d_cos, st->d_sin, pool(st, l),
-                 c.T, m.n_heads, m.n_kv_heads, D, st->opts.max_ctx};
-    return rope_kv(a, s, i);
-  });
-  if (r != HS_OK) return r;
+  // a decode step rotates and appends inside the attention kernel
+  if (!c.decode) {
+    r = run(st, s, "rope_kv", [&](LaunchInfo* i) {
+      RopeKvArgs a{st->w_qkv, NQKV, c.pos, c.slot, st->d_cos, st->d_sin, pool(st, l),
+                   c.T, m.n_heads, m.n_kv_heads, D, st->opts.max_ctx};
+      return rope_kv(a, s, i);
+    });
+    if (r != HS_OK) return r;
+  }
   if (!c.decode) {
     r = run(st, s, "attn", [&](LaunchInfo* i) {
       AttnPrefillArgs a{st->w_qkv, NQKV, st->w_attn, QD, c.cu, c.tiles, c.n_tiles,
@@ -432,6 +435,10 @@ hs_status layer_forward(hs_stage* st, int l, bf16_t* x, const LayerCall& c, hipS
       AttnDecodeArgs a{st->w_qkv, NQKV, pool(st, l), c.bt, c.ctx, st->w_part_o, st->w_part_ml,
                        st->w_attn, QD, c.T, m.n_heads, m.n_kv_heads, D, st->max_blocks_per_seq,
                        st->max_splits, c.call_splits, c.kv_read_bytes};
+      a.pool_w = pool(st, l);
+      a.cos_t = st->d_cos;
+      a.sin_t = st->d_sin;
+      a.max_pos = st->opts.max_ctx;
       return attn_decode(a, s, i);
     });
   }

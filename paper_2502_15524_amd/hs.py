@@ -117,6 +117,9 @@ _SIGS = {
     "hs_k_rmsnorm": [_P, _P, _P, C.c_int32, C.c_int32, C.c_float, _P],
     "hs_k_attn_decode": [_P, C.c_int64, _P, _P, _P, _P, C.c_int64, C.c_int32, C.c_int32,
                          C.c_int32, C.c_int32, C.c_int32, C.c_int32, _P],
+    "hs_k_attn_decode_rope": [_P, C.c_int64, _P, _P, _P, _P, _P, C.c_int32, _P, C.c_int64,
+                              C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                              _P],
 }
 EXPORTED = sorted(list(_SIGS) + ["hs_last_error"])
 
@@ -369,6 +372,16 @@ def hs_k_attn_decode(q, ldq, pool, block_table, ctx, out, ldo, B, n_heads, n_kv_
     """Decode attention over a paged KV pool; block_table and ctx are device pointers."""
     _check(lib().hs_k_attn_decode(q, ldq, pool, block_table, ctx, out, ldo, B, n_heads,
                                   n_kv_heads, head_dim, max_blocks, max_ctx, stream or None))
+
+
+def hs_k_attn_decode_rope(qkv, ldqkv, pool, block_table, ctx, cos_t, sin_t, max_pos, out, ldo,
+                          B, n_heads, n_kv_heads, head_dim, max_blocks, max_ctx, stream=0):
+    """Decode attention with the step's RoPE and cache append folded in: qkv
+    holds the new tokens' projections before RoPE; the rotated key and the
+    value are written into the pool slot of position ctx - 1."""
+    _check(lib().hs_k_attn_decode_rope(qkv, ldqkv, pool, block_table, ctx, cos_t, sin_t,
+                                       max_pos, out, ldo, B, n_heads, n_kv_heads, head_dim,
+                                       max_blocks, max_ctx, stream or None))
 
 
 def hs_k_rmsnorm(x, g, out, rows, hidden, eps, stream=0):

@@ -4,7 +4,7 @@ functions where it has them)."""
 import numpy as np
 import pytest
 
-from oracle.llama import attention, rms_norm, silu
+from oracle.llama import apply_rope, attention, rms_norm, rope_angles, silu
 from workloads import gen
 from tests import gpu_util as G
 
@@ -229,6 +229,75 @@ def test_attn_decode(lens, nh, nkv, d):
                         vs[i].astype(np.float64), [n - 1], np.arange(n))[0]
         err = np.abs(outs[0][i] - ref).max()
         assert err <= 2e-2 * np.abs(ref).max() + 1e-3, (i, err)
+
+
+@pytest.mark.parametrize("lens,nh,nkv,d", [
+    ([1], 4, 4, 64), ([17, 300, 64, 65], 4, 4, 64), ([5, 130, 1100, 64, 2100], 32, 8, 128),
+    ([512], 32, 32, 128), ([1000, 33, 16], 16, 4, 64), ([80, 64, 63, 2], 8, 2, 128)])
+def test_attn_decode_rope(lens, nh, nkv, d):
+    """Decode attention with the step's RoPE and cache append folded in. The
+    last position of each sequence is the new token, given before RoPE in a
+    QKV row (its pool slot holds garbage that must not be read); against the
+    oracle's RoPE and attention, and the appended slot against the rotated
+    key (one bf16 rounding) and the value (bitwise)."""
+    torch = G.torch()
+    hs = _hs()
+    q0, pool, table, ks, vs = _paged_case(lens, nh, nkv, d, sum(lens) + 7 * nh)
+    rng = np.random.default_rng(len(lens) * 31 + d)
+    B, ldqkv, max_ctx = len(lens), (nh + 2 * nkv) * d, max(lens)
+    qkv = gen.round_to_bf16((rng.standard_normal((B, ldqkv)) * 1.5).astype(np.float32))
+    for i, n in enumerate(lens):
+        pool[table[i, (n - 1) // 16], :, :, (n - 1) % 16] = 4096.0
+    cos, sin = rope_angles(np.arange(max_ctx), d, 10000.0)
+    dcos = torch.from_numpy(np.ascontiguousarray(cos.astype(np.float32))).cuda()
+    dsin = torch.from_numpy(np.ascontiguousarray(sin.astype(np.float32))).cuda()
+    dqkv = G.to_dev_bf16(qkv)
+    dpool = G.to_dev_bf16(pool.reshape(-1))
+    dtab = torch.from_numpy(table).cuda()
+    dctx = torch.tensor(lens, dtype=torch.int32).cuda()
+    out = torch.zeros((B, nh * d), dtype=torch.bfloat16, device="cuda")
+    hs.hs_k_attn_decode_rope(dqkv.data_ptr(), ldqkv, dpool.data_ptr(), dtab.data_ptr(),
+                             dctx.data_ptr(), dcos.data_ptr(), dsin.data_ptr(), max_ctx,
+                             out.data_ptr(), nh * d, B, nh, nkv, d, table.shape[1], max_ctx,
+                             G.stream_ptr())
+    torch.cuda.synchronize()
+    got = G.from_dev_bf16(out)
+    pool_after = G.from_dev_bf16(dpool).reshape(pool.shape)
+    pool_bits = gen.to_bf16_bits(pool_after)
+    for i, n in enumerate(lens):
+        c, s_ = cos[n - 1:n], sin[n - 1:n]
+        qr = apply_rope(qkv[i, :nh * d].reshape(1, nh, d).astype(np.float64), c, s_)
+        kr = apply_rope(qkv[i, nh * d:(nh + nkv) * d].reshape(1, nkv, d).astype(np.float64), c, s_)
+        v_new = qkv[i, (nh + nkv) * d:].reshape(1, nkv, d)
+        blk, off = table[i, (n - 1) // 16], (n - 1) % 16
+        k_slot = pool_after[blk, 0, :, off]
+        assert np.abs(k_slot - kr[0]).max() <= 8e-3 * np.abs(kr).max(), i
+        assert np.array_equal(pool_bits[blk, 1, :, off], gen.to_bf16_bits(v_new[0])), i
+        K = np.concatenate([ks[i][:n - 1], k_slot[None]]).astype(np.float64)
+        V = np.concatenate([vs[i][:n - 1], v_new]).astype(np.float64)
+        ref = attention(qr, K, V, [n - 1], np.arange(n))[0]
+        err = np.abs(got[i] - ref).max()
+        assert err <= 2e-2 * np.abs(ref).max() + 1e-3, (i, err)
+    # the cached tokens before the new one are untouched
+    keep = np.ones(pool.shape[:1] + pool.shape[3:4], bool)
+    for i, n in enumerate(lens):
+        keep[table[i, (n - 1) // 16], (n - 1) % 16] = False
+    before = gen.to_bf16_bits(pool.transpose(0, 3, 1, 2, 4))[keep]
+    after = pool_bits.transpose(0, 3, 1, 2, 4)[keep]
+    assert np.array_equal(before, after)
+
+
+def test_attn_decode_rope_rejects_short_tables():
+    torch = G.torch()
+    hs = _hs()
+    buf = torch.zeros(1 << 16, dtype=torch.int32, device="cuda")
+    p = buf.data_ptr()
+    with pytest.raises(hs.HSError) as e:      # max_pos < max_ctx
+        hs.hs_k_attn_decode_rope(p, 384, p, p, p, p, p, 16, p, 128, 1, 1, 1, 128, 2, 32)
+    assert e.value.code == hs.HS_EINVAL
+    with pytest.raises(hs.HSError) as e:      # QKV rows narrower than the heads
+        hs.hs_k_attn_decode_rope(p, 256, p, p, p, p, p, 32, p, 128, 1, 1, 1, 128, 2, 32)
+    assert e.value.code == hs.HS_EINVAL
 
 
 @pytest.mark.parametrize("rows,hidden", [(1, 256), (37, 4096), (5, 5120), (3, 8192)])
