@@ -104,8 +104,11 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_kernel(AttnPrefillArgs a
         const uint32_t ev = mine ^ ((mine ^ other) & odd);   // even key's word
         const uint32_t od = other ^ ((other ^ mine) & odd);  // odd key's word
         const int col = lcol + (key & 1) * 4 + 2 * e;
-        sVt[col * LVW + word] = (ev & 0xFFFFu) | (od << 16);
-        sVt[(col + 1) * LVW + word] = (ev >> 16) | (od & 0xFFFF0000u);
+        // 16-byte chunks of a row XOR-swizzled by the row's 16-row group:
+        // the 16 column groups of a store then hit distinct banks
+        sVt[col * LVW + (word ^ (((col >> 4) & 7) << 2))] = (ev & 0xFFFFu) | (od << 16);
+        sVt[(col + 1) * LVW + (word ^ ((((col + 1) >> 4) & 7) << 2))] =
+            (ev >> 16) | (od & 0xFFFF0000u);
       }
     }
     __syncthreads();
@@ -162,7 +165,7 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_kernel(AttnPrefillArgs a
       const bf16x8_v pf = as_bf16x8(pb);
 #pragma unroll
       for (int dt = 0; dt < D / 16; ++dt) {
-        const pack8 vb = ld16(&sVt[(dt * 16 + fr) * LVW + st * 16 + g * 4]);
+        const pack8 vb = ld16(&sVt[(dt * 16 + fr) * LVW + (((st * 4 + g) ^ (dt & 7)) << 2)]);
         o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vb), pf, o[dt], 0, 0, 0);
       }
     }
