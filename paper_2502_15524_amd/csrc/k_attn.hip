@@ -19,8 +19,14 @@ namespace hs {
 // scores of ONE query (4 per 16-key subtile); the softmax statistics of a
 // query then live in the 4 lanes l, l+16, l+32, l+48. P^T feeds the second
 // MFMA as its B operand with the key order of each 32-key step permuted
-// (lane group g, element e -> key 4g+e for e<4, 16+4g+e-4 otherwise); V^T is
-// stored in LDS in that permuted order, so the product is unchanged.
+// (lane group g, element e -> key 4g+e for e<4, 16+4g+e-4 otherwise). K and
+// V are both staged row-major ([key][d]); the V^T fragments of the second
+// MFMA come from transposing LDS reads (ds_read_b64_tr_b16: within each
+// 16-lane group, lane o receives element o % 4 of the 4-element rows
+// addressed by lanes o / 4, o / 4 + 4, o / 4 + 8 and o / 4 + 12), two per
+// fragment, whose row addresses follow the same key permutation.
+
+typedef short s16x4_v __attribute__((ext_vector_type(4)));
 
 template <int D, int NW>
 __global__ __launch_bounds__(64 * NW) void attn_prefill_kernel(AttnPrefillArgs a, float scale_log2) {
@@ -28,14 +34,14 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_kernel(AttnPrefillArgs a
   constexpr int QT = 16 * NW;   // queries per workgroup
   constexpr int KB = 64;        // keys per block
   constexpr int LK = D + 8;     // padded K row in LDS
-  constexpr int LVW = KB / 2 + 4;  // V^T row in 32-bit words (key pairs): 16-byte aligned,
-                                   // the 16 rows of a fragment on distinct banks
+  constexpr int LV = D + 16;     // padded V row in LDS: the 8-byte rows of a transposing
+                                // read (4 keys x 4 column quads per 16 lanes) on distinct banks
   constexpr int CPK = D / 8;    // 16-byte chunks per key row
   constexpr int KPP = NT / CPK; // key rows per load pass
   constexpr int PASS = KB / KPP;
   static_assert(KB % KPP == 0 && (KPP % 2) == 0, "load mapping");
   __shared__ __attribute__((aligned(16))) bf16_t sK[KB * LK];
-  __shared__ __attribute__((aligned(16))) uint32_t sVt[D * LVW];
+  __shared__ __attribute__((aligned(16))) bf16_t sV[KB * LV];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int seq = a.tiles[2 * blockIdx.x], q0 = a.tiles[2 * blockIdx.x + 1];
@@ -83,33 +89,7 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_kernel(AttnPrefillArgs a
     for (int p = 0; p < PASS; ++p) {
       const int key = p * KPP + lkey;
       st16(&sK[key * LK + lcol], kreg[p]);
-      // V^T: keys (2j, 2j+1) sit in lanes L and L ^ CPK; the even-key lane
-      // writes columns lcol..+3 and the odd-key lane lcol+4..+7, each as
-      // 4-byte (key pair) words. Within each 32-key half of a row the pairs
-      // are stored in the order the PV MFMA's lane groups read them (group
-      // g: keys 4g..4g+3 and 16+4g..16+4g+3), so a fragment is one 16-byte
-      // read.
-      uint32_t pw[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) pw[e] = __shfl_xor(vreg[p].w[e], CPK, 64);
-      // selections by bit mask (all ones for an odd key): with a ternary the
-      // compiler turns the pick into a runtime index into scratch memory
-      const uint32_t odd = 0u - (uint32_t)(key & 1);
-      const int kp = key >> 1, j = kp & 15;
-      const int word = (kp >> 4) * 16 + ((j & 7) >> 1) * 4 + (j >> 3) * 2 + (j & 1);
-#pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        const uint32_t mine = vreg[p].w[e] ^ ((vreg[p].w[e] ^ vreg[p].w[2 + e]) & odd);
-        const uint32_t other = pw[e] ^ ((pw[e] ^ pw[2 + e]) & odd);
-        const uint32_t ev = mine ^ ((mine ^ other) & odd);   // even key's word
-        const uint32_t od = other ^ ((other ^ mine) & odd);  // odd key's word
-        const int col = lcol + (key & 1) * 4 + 2 * e;
-        // 16-byte chunks of a row XOR-swizzled by the row's 16-row group:
-        // the 16 column groups of a store then hit distinct banks
-        sVt[col * LVW + (word ^ (((col >> 4) & 7) << 2))] = (ev & 0xFFFFu) | (od << 16);
-        sVt[(col + 1) * LVW + (word ^ ((((col + 1) >> 4) & 7) << 2))] =
-            (ev >> 16) | (od & 0xFFFF0000u);
-      }
+      st16(&sV[key * LV + lcol], vreg[p]);
     }
     __syncthreads();
     if (kb + 1 < n_kb) fetch(kb + 1);  // in flight during this block's MFMAs
@@ -125,21 +105,29 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_kernel(AttnPrefillArgs a
         s[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ks], s[t], 0, 0, 0);
       }
     }
+    // Scores stay unscaled: the running max is kept in the scaled (log2)
+    // domain and a probability is one FMA and one exp2. Only a block that
+    // reaches past this wave's first query or the sequence end is masked.
     float bmax = -INFINITY;
+    if (k0 + KB - 1 > qw0 || k0 + KB > len) {  // uniform across the wave
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
+      for (int t = 0; t < 4; ++t)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int key = k0 + t * 16 + g * 4 + e;
-        float v = s[t][e] * scale_log2;
-        if (key > qrow || key >= len) v = -INFINITY;
-        s[t][e] = v;
-        bmax = fmaxf(bmax, v);
-      }
+        for (int e = 0; e < 4; ++e) {
+          const int key = k0 + t * 16 + g * 4 + e;
+          if (key > qrow || key >= len) s[t][e] = -INFINITY;
+          bmax = fmaxf(bmax, s[t][e]);
+        }
+    } else {
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) bmax = fmaxf(bmax, s[t][e]);
+    }
     bmax = fmaxf(bmax, __shfl_xor(bmax, 16, 64));
     bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
     // finite: every wave processes block 0 and every query sees key 0
-    const float m_new = fmaxf(m_run, bmax);
+    const float m_new = fmaxf(m_run, bmax * scale_log2);
     const float corr = fast_exp2(m_run - m_new);
     m_run = m_new;
     float psum = 0.f;
@@ -147,7 +135,7 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_kernel(AttnPrefillArgs a
     for (int t = 0; t < 4; ++t)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float p = fast_exp2(s[t][e] - m_new);
+        const float p = fast_exp2(__builtin_fmaf(s[t][e], scale_log2, -m_new));
         s[t][e] = p;
         psum += p;
       }
@@ -165,8 +153,17 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_kernel(AttnPrefillArgs a
       const bf16x8_v pf = as_bf16x8(pb);
 #pragma unroll
       for (int dt = 0; dt < D / 16; ++dt) {
-        const pack8 vb = ld16(&sVt[(dt * 16 + fr) * LVW + (((st * 4 + g) ^ (dt & 7)) << 2)]);
-        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vb), pf, o[dt], 0, 0, 0);
+        // rows of keys 32 st + 4g + (fr / 4) and 32 st + 16 + 4g + (fr / 4),
+        // columns 16 dt + 4 (fr % 4) .. + 3: lane (fr, g) receives column
+        // 16 dt + fr of keys 32 st + 4g + 0..3 and 32 st + 16 + 4g + 0..3
+        const bf16_t* vp = &sV[(st * 32 + 4 * g + (fr >> 2)) * LV + dt * 16 + 4 * (fr & 3)];
+        const s16x4_v v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s16x4_v*)(vp));
+        const s16x4_v v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s16x4_v*)(vp + 16 * LV));
+        const bf16x8_v vb = __builtin_bit_cast(
+            bf16x8_v, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb, pf, o[dt], 0, 0, 0);
       }
     }
   }
