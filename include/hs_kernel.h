@@ -66,7 +66,7 @@ hs_status hs_k_attn_prefill(const void* qkv, void* out, const int32_t* cu_seqlen
  * ctx: device int32 [B], cached tokens of each sequence including the new
  * one (1 <= ctx <= max_ctx); out: bf16 [B][ldo], head h at column
  * h * head_dim. max_ctx (host) sizes the launch. The context is processed in
- * fixed 64-token splits whose partial results go through a workspace that
+ * fixed 128-token splits whose partial results go through a workspace that
  * the library allocates per device on first use and grows when needed
  * (calls on one device must not overlap); the call is asynchronous on
  * `stream` and deterministic. */

@@ -76,7 +76,7 @@ hipError_t attn_prefill(const AttnPrefillArgs& a, hipStream_t s, LaunchInfo* inf
 // 128-query tiles (summed over sequences) and n_heads heads.
 int attn_prefill_waves(int64_t tiles_of_128, int n_heads);
 
-constexpr int kDecodeSplit = 64;   // tokens per split of the decode attention
+constexpr int kDecodeSplit = 128;  // tokens per split of the decode attention
 
 struct AttnDecodeArgs {
   const bf16_t* q; int64_t ldq;   // [B][ldq], query heads at column h * D

@@ -3,7 +3,7 @@
 // Prefill reads post-RoPE q, k and v straight from the QKV GEMM output (the
 // whole prompt is in the call), one workgroup per (64-query tile, head).
 // Decode reads the paged KV pools through each sequence's block table; the
-// context is cut into fixed 64-token splits, so the split count depends on
+// context is cut into fixed 128-token splits, so the split count depends on
 // the context length only and the result is deterministic.
 #include "hs_device.h"
 #include "hs_kernels.h"
@@ -211,10 +211,11 @@ int attn_prefill_waves(int64_t tiles_of_128, int n_heads) {
 
 // ------------------------------------------------------------------- decode
 //
-// The context of a sequence is cut into fixed 64-token splits; one
+// The context of a sequence is cut into fixed 128-token splits; one
 // workgroup per (split, kv head, sequence). D/8 lanes share a token (one
 // 16-byte chunk of its key and value rows each), so 256 threads cover
-// 2048/D tokens per pass and every thread sees 4 tokens of the split. Per
+// 2048/D tokens per pass and every thread sees 8 (D = 128) or 4 (D = 64)
+// tokens of the split. Per
 // group of 4 tokens a thread forms the G scores (partial dot products summed
 // over the token's lanes with DPP row operations), then updates its online
 // softmax once: new max, one rescale of the accumulators, four
@@ -339,7 +340,7 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a
   static_assert(LPT == 16 || LPT == 8, "head dim 128 or 64");
   static_assert(TPP == 16 || TPP == 32, "one or two cache blocks per pass");
   constexpr int BPS = kDecodeSplit / 16;  // cache blocks per split
-  static_assert(BPS == 4, "split of four cache blocks");
+  static_assert(BPS * 16 == kDecodeSplit && PASSES * TPP == kDecodeSplit, "split of whole blocks");
   __shared__ float s_ml[4][G][2];
   __shared__ float s_acc[4][G][D];
 
@@ -351,7 +352,8 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a
 #pragma unroll
   for (int j = 0; j < BPS; ++j) phys[j] = bt[min(split * BPS + j, a.max_blocks - 1)];  // past: unused
   const int ctx = a.ctx[b];
-  asm volatile("" ::"s"(phys[0]), "s"(phys[1]), "s"(phys[2]), "s"(phys[3]));  // not sunk below the branch
+#pragma unroll
+  for (int j = 0; j < BPS; ++j) asm volatile("" ::"s"(phys[j]));  // not sunk below the branch
   const int t_begin = split * kDecodeSplit;
   if (t_begin >= ctx) return;  // uniform across the workgroup
   const int tid = threadIdx.x, tl = tid / LPT, c = tid % LPT;
@@ -426,7 +428,9 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a
       if (tl == t_new % TPP) {
         kv[p] = kr;
         const int blk = t_new / 16;
-        const int ph = blk == 0 ? phys[0] : blk == 1 ? phys[1] : blk == 2 ? phys[2] : phys[3];
+        int ph = phys[0];
+#pragma unroll
+        for (int j = 1; j < BPS; ++j) ph = blk == j ? phys[j] : ph;
         bf16_t* kd = a.pool_w + ((int64_t)ph * 2 * a.n_kv_heads + kh) * 16 * D +
                      ((ctx - 1) & 15) * D + c * 8;
         st16(kd, kr);
