@@ -649,7 +649,7 @@ hipError_t dispatch_epi_skinny(const GemmArgs& a, int epi, hipStream_t s) {
 // 16, slabs unrolled per wave, waves per workgroup): the ones the selection
 // in gemm() takes.
 #define HS_SKINNY_MCH1(X) \
-  X(1, 1, 8) X(1, 2, 8) X(2, 1, 8) X(2, 1, 4) X(4, 1, 4) X(2, 1, 2) X(4, 1, 2) X(8, 1, 2)
+  X(1, 1, 8) X(1, 2, 8) X(2, 1, 8) X(2, 1, 4) X(4, 1, 4) X(2, 1, 2) X(4, 1, 2) X(8, 1, 2) X(1, 1, 16)
 
 hipError_t dispatch_skinny1(const GemmArgs& a, int epi, int nf, int u, int wv, hipStream_t s) {
 #define HS_SKINNY_CASE(NF_, U_, WV_) \
@@ -742,7 +742,8 @@ hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info) {
     // workgroup (WV) for one token chunk, from a sweep on MI355X over the
     // decode projections of 7B, 8B and 13B models at 1, 4, 8 and 16 tokens:
     // narrow outputs (o, down, QKV up to 8192 wide) fill the chip with eight
-    // waves per workgroup, wide QKV and gate/up with four; gate/up takes four
+    // waves per workgroup (sixteen for a 4096 x 4096 o projection), wide QKV
+    // and gate/up with four; gate/up takes four
     // row tiles per workgroup once that still gives 1.5 workgroups per CU
     // (8B, 13B: 38 and 45 instead of 43 and 52 us); o/down wider than one
     // row tile per CU take one slab per group up to 4 tokens and two row
@@ -762,6 +763,7 @@ hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info) {
     } else if (epi == EPI_RESID) {
       wv = 8;
       if (a.N / 16 > cus) nf = a.M > 4 ? 2 : 1;
+      else if (a.K <= 4096) wv = 16;  // 4096 x 4096 o projection: 9.4 -> 8.2 us at 8 tokens
       else u = a.M <= 8 ? 2 : 1;
     } else if (epi == EPI_STORE) {
       nf = 2, wv = a.N <= 8192 ? 8 : 4;
