@@ -8,6 +8,9 @@
 #include "hs_device.h"
 #include "hs_kernels.h"
 
+#include <stdlib.h>
+#include <string.h>
+
 #include <algorithm>
 
 namespace hs {
@@ -540,6 +543,222 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a
   }
 }
 
+// MFMA form of the split kernel for grouped-query heads (G >= 2, D = 128).
+// Wave w takes tokens 32w .. 32w + 31 of the split (two cache blocks).
+// Scores are formed transposed, S^T = K Q^T, with 16x16x32 MFMAs: the keys
+// on the rows (lane (r, g) loads key r of a block, d-chunk g of each 32-d
+// step, straight from the pool) and the G query heads of the kv head on the
+// columns (the other columns zero), so lane (r, g) ends with the scores of
+// keys 4g .. 4g+3 (and 16 + 4g .. 16 + 4g + 3) for query head r. The values
+// are staged row-major in the wave's LDS buffer and P V^T reads its V^T
+// fragments with transposing LDS reads (as the prefill kernel does); the
+// probabilities are the B operand exactly as the score MFMAs left them.
+// With fused RoPE the rotation pairs (d, d + D/2) sit in one lane. The
+// waves' partial results are merged through LDS in wave order.
+typedef short s16x4_dv __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void rope_pair(pack8& x1, pack8& x2, const float* cs, const float* sn) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float a0 = lo_bf(x1.w[e]), a1 = hi_bf(x1.w[e]);
+    const float b0 = lo_bf(x2.w[e]), b1 = hi_bf(x2.w[e]);
+    const float c0 = cs[2 * e], c1 = cs[2 * e + 1], s0 = sn[2 * e], s1 = sn[2 * e + 1];
+    x1.w[e] = pack2bf(a0 * c0 - b0 * s0, a1 * c1 - b1 * s1);
+    x2.w[e] = pack2bf(b0 * c0 + a0 * s0, b1 * c1 + a1 * s1);
+  }
+}
+
+template <int G, bool ROPE>
+__global__ __launch_bounds__(256) void attn_decode_gqa_kernel(AttnDecodeArgs a, float scale_log2) {
+  constexpr int D = 128;
+  static_assert(G >= 2 && G <= 16, "the query heads of a kv head fit the 16 MFMA columns");
+  static_assert(kDecodeSplit == 128, "four waves of two cache blocks");
+  constexpr int KS = D / 32;      // 32-d steps of the score MFMAs; value chunks per lane per block
+  constexpr int DT = D / 16;      // 16-row tiles of d in the P V MFMAs
+  constexpr int LV = D + 16;      // padded V row (transposing reads on distinct banks)
+  constexpr int BPS = kDecodeSplit / 16;
+  __shared__ __attribute__((aligned(16))) bf16_t sV[4][32 * LV];
+  __shared__ float s_ml[4][G][2];
+  __shared__ __attribute__((aligned(16))) float s_acc[4][G][D];
+
+  const int split = blockIdx.x, kh = blockIdx.y, b = blockIdx.z;
+  const int32_t* bt = a.block_table + (int64_t)b * a.max_blocks;
+  int phys[BPS];
+#pragma unroll
+  for (int j = 0; j < BPS; ++j) phys[j] = bt[min(split * BPS + j, a.max_blocks - 1)];  // past: unused
+  const int ctx = a.ctx[b];
+#pragma unroll
+  for (int j = 0; j < BPS; ++j) asm volatile("" ::"s"(phys[j]));  // not sunk below the branch
+  const int t_begin = split * kDecodeSplit;
+  if (t_begin >= ctx) return;  // uniform across the workgroup
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int fr = lane & 15, g = lane >> 4;
+  const int h0 = kh * G;
+  const int64_t kv_stride = (int64_t)a.n_kv_heads * 16 * D;  // K block -> V block
+  const bf16_t* qrow = a.q + (int64_t)b * a.ldq;
+  const int tb = t_begin + wave * 32;  // first token of this wave
+
+  pack8 kf[2][KS], vf[2][KS], qf[KS];
+  bool live[2], is_new[2];
+  int ph[2];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int blk = wave * 2 + t;
+    int p = phys[0];
+#pragma unroll
+    for (int j = 1; j < BPS; ++j) p = blk == j ? phys[j] : p;
+    ph[t] = p;
+    const int tok = tb + 16 * t + fr;
+    live[t] = tok < ctx;
+    is_new[t] = ROPE && tok == ctx - 1;
+    const bf16_t* krow = a.pool + ((int64_t)p * 2 * a.n_kv_heads + kh) * 16 * D + fr * D;
+    const bf16_t* vrow = krow + kv_stride;
+    if (is_new[t]) {  // not in the pool yet: the projection's rows
+      krow = qrow + (int64_t)(a.n_heads + kh) * D;
+      vrow = qrow + (int64_t)(a.n_heads + a.n_kv_heads + kh) * D;
+    }
+    // all key and value loads go out first (non-temporal: each cached byte
+    // is read once per step)
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      kf[t][ks] = live[t] ? ld16_nt(krow + ks * 32 + g * 8) : zero8();
+      vf[t][ks] = live[t] ? ld16_nt(vrow + ks * 32 + g * 8) : zero8();
+    }
+  }
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks)
+    qf[ks] = fr < G ? ld16(qrow + (h0 + fr) * D + ks * 32 + g * 8) : zero8();
+  if constexpr (ROPE) {
+    // lane (r, g) holds d = 32 ks + 8 g + e; its pair partners d + D/2 are
+    // chunk ks + KS/2 of the same lane
+    const float* ct = a.cos_t + (int64_t)(ctx - 1) * (D / 2);
+    const float* st = a.sin_t + (int64_t)(ctx - 1) * (D / 2);
+#pragma unroll
+    for (int ks = 0; ks < KS / 2; ++ks) {
+      float cs[8], sn[8];
+#pragma unroll
+      for (int e = 0; e < 8; e += 4) {
+        const float4 cv = *reinterpret_cast<const float4*>(ct + ks * 32 + g * 8 + e);
+        const float4 sv = *reinterpret_cast<const float4*>(st + ks * 32 + g * 8 + e);
+        cs[e] = cv.x;
+        cs[e + 1] = cv.y;
+        cs[e + 2] = cv.z;
+        cs[e + 3] = cv.w;
+        sn[e] = sv.x;
+        sn[e + 1] = sv.y;
+        sn[e + 2] = sv.z;
+        sn[e + 3] = sv.w;
+      }
+      rope_pair(qf[ks], qf[ks + KS / 2], cs, sn);
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+        if (is_new[t]) rope_pair(kf[t][ks], kf[t][ks + KS / 2], cs, sn);
+    }
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+      if (is_new[t]) {  // append the rotated key and the value to the cache
+        bf16_t* kd = a.pool_w + ((int64_t)ph[t] * 2 * a.n_kv_heads + kh) * 16 * D + fr * D;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          st16(kd + ks * 32 + g * 8, kf[t][ks]);
+          st16(kd + kv_stride + ks * 32 + g * 8, vf[t][ks]);
+        }
+      }
+  }
+
+  // values row-major into this wave's buffer (key 16 t + r, chunk 4 ks + g)
+  bf16_t* sv = sV[wave];
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) st16(sv + (16 * t + fr) * LV + ks * 32 + g * 8, vf[t][ks]);
+
+  // S^T: lane (r, g) gets keys tb + 16 t + 4g + j of query head r
+  f32x4_v s[2];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    s[t] = f32x4_v{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      s[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kf[t][ks]), as_bf16x8(qf[ks]), s[t], 0, 0, 0);
+  }
+  float m = -INFINITY;
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (tb + 16 * t + 4 * g + j >= ctx) s[t][j] = -INFINITY;
+      m = fmaxf(m, s[t][j]);
+    }
+  m = fmaxf(m, __shfl_xor(m, 16, 64));
+  m = fmaxf(m, __shfl_xor(m, 32, 64));
+  const float ms = m * scale_log2;  // running max in the scaled (log2) domain
+  float l = 0.f;
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      s[t][j] = m == -INFINITY ? 0.f : fast_exp2(__builtin_fmaf(s[t][j], scale_log2, -ms));
+      l += s[t][j];
+    }
+  l += __shfl_xor(l, 16, 64);
+  l += __shfl_xor(l, 32, 64);
+  pack8 pk;
+  pk.w[0] = pack2bf(s[0][0], s[0][1]);
+  pk.w[1] = pack2bf(s[0][2], s[0][3]);
+  pk.w[2] = pack2bf(s[1][0], s[1][1]);
+  pk.w[3] = pack2bf(s[1][2], s[1][3]);
+  const bf16x8_v pf = as_bf16x8(pk);
+  asm volatile("" ::: "memory");  // the value stores (this wave's) before the fragment reads
+  // O^T = V^T P^T: lane (r, g) gets rows d = 16 dt + 4g + j of query head r
+  f32x4_v o[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) {
+    const bf16_t* vp = sv + (4 * g + (fr >> 2)) * LV + dt * 16 + 4 * (fr & 3);
+    const s16x4_dv v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) s16x4_dv*)(vp));
+    const s16x4_dv v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) s16x4_dv*)(vp + 16 * LV));
+    const bf16x8_v vb =
+        __builtin_bit_cast(bf16x8_v, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+    o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb, pf, f32x4_v{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+  }
+
+  if (fr < G) {
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+      *reinterpret_cast<f32x4_v*>(&s_acc[wave][fr][dt * 16 + 4 * g]) = o[dt];
+    if (g == 0) {
+      s_ml[wave][fr][0] = ms;
+      s_ml[wave][fr][1] = l;
+    }
+  }
+  __syncthreads();
+  // partials of this (sequence, kv head): [G][max_splits][D] and [G][max_splits][2]
+  const int64_t base = ((int64_t)b * a.n_heads + h0) * a.max_splits;
+  for (int i = tid; i < G * D; i += 256) {
+    const int gg = i / D, d = i % D;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, s_ml[w][gg][0]);
+    float L = 0.f, O = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float mw = s_ml[w][gg][0];
+      if (mw == -INFINITY) continue;
+      const float f = fast_exp2(mw - M);
+      L += s_ml[w][gg][1] * f;
+      O += s_acc[w][gg][d] * f;
+    }
+    const int64_t row = base + gg * a.max_splits + split;
+    a.part_o[row * D + d] = O;
+    if (d == 0) {
+      a.part_ml[row * 2] = M;
+      a.part_ml[row * 2 + 1] = L;
+    }
+  }
+}
+
 // Merge of the splits of every (query head, sequence).
 template <int D>
 __global__ __launch_bounds__(D) void attn_decode_combine_kernel(AttnDecodeArgs a) {
@@ -557,6 +776,16 @@ namespace {
 template <int D, int G>
 void launch_split(const AttnDecodeArgs& a, float sl, hipStream_t s) {
   dim3 grid(a.call_splits, a.n_kv_heads, a.B);
+  static const char* force = getenv("HS_DECODE_ATTN");  // "valu" (tuning only)
+  if constexpr (D == 128 && G >= 2) {
+    if (!(force && strcmp(force, "valu") == 0)) {
+      if (a.pool_w)
+        hipLaunchKernelGGL((attn_decode_gqa_kernel<G, true>), grid, dim3(256), 0, s, a, sl);
+      else
+        hipLaunchKernelGGL((attn_decode_gqa_kernel<G, false>), grid, dim3(256), 0, s, a, sl);
+      return;
+    }
+  }
   if (a.pool_w)
     hipLaunchKernelGGL((attn_decode_split_kernel<D, G, true>), grid, dim3(256), 0, s, a, sl);
   else
