@@ -205,7 +205,8 @@ def test_attn_decode_batch_invariant():
 
 @pytest.mark.parametrize("lens,nh,nkv,d", [
     ([1], 4, 4, 64), ([17, 300, 64, 65], 4, 4, 64), ([5, 130, 1100, 64, 2100], 32, 8, 128),
-    ([512], 32, 32, 128), ([2, 129, 700], 8, 2, 128), ([1000, 33], 16, 4, 64)])
+    ([512], 32, 32, 128), ([2, 129, 700], 8, 2, 128), ([1000, 33], 16, 4, 64),
+    ([300, 17, 129], 8, 4, 128)])   # two query heads per kv head
 def test_attn_decode(lens, nh, nkv, d):
     """One query per sequence (at position ctx - 1) over a paged cache, against
     the oracle's attention; a second call gives the same bits."""
@@ -234,7 +235,8 @@ def test_attn_decode(lens, nh, nkv, d):
 
 @pytest.mark.parametrize("lens,nh,nkv,d", [
     ([1], 4, 4, 64), ([17, 300, 64, 65], 4, 4, 64), ([5, 130, 1100, 64, 2100], 32, 8, 128),
-    ([512], 32, 32, 128), ([1000, 33, 16], 16, 4, 64), ([80, 64, 63, 2], 8, 2, 128)])
+    ([512], 32, 32, 128), ([1000, 33, 16], 16, 4, 64), ([80, 64, 63, 2], 8, 2, 128),
+    ([300, 17, 129], 8, 4, 128)])
 def test_attn_decode_rope(lens, nh, nkv, d):
     """Decode attention with the step's RoPE and cache append folded in. The
     last position of each sequence is the new token, given before RoPE in a
