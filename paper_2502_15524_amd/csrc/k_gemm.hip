@@ -649,7 +649,8 @@ hipError_t dispatch_epi_skinny(const GemmArgs& a, int epi, hipStream_t s) {
 // 16, slabs unrolled per wave, waves per workgroup): the ones the selection
 // in gemm() takes.
 #define HS_SKINNY_MCH1(X) \
-  X(1, 1, 8) X(1, 2, 8) X(2, 1, 8) X(2, 1, 4) X(4, 1, 4) X(2, 1, 2) X(4, 1, 2) X(8, 1, 2) X(1, 1, 16)
+  X(1, 1, 8) X(1, 2, 8) X(2, 1, 8) X(2, 1, 4) X(4, 1, 4) X(2, 1, 2) X(4, 1, 2) X(8, 1, 2) X(1, 1, 16) \
+  X(3, 1, 16)
 
 hipError_t dispatch_skinny1(const GemmArgs& a, int epi, int nf, int u, int wv, hipStream_t s) {
 #define HS_SKINNY_CASE(NF_, U_, WV_) \
@@ -767,6 +768,9 @@ hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info) {
       else u = a.M <= 8 ? 2 : 1;
     } else if (epi == EPI_STORE) {
       nf = 2, wv = a.N <= 8192 ? 8 : 4;
+      // three row tiles when that gives one workgroup per CU (7B QKV: 256 x
+      // 48 rows; 21.5 -> 19.5 us)
+      if (a.N % 48 == 0 && a.N / 48 <= cus && a.N / 48 > cus * 3 / 4) nf = 3, wv = 16;
     }
     if (force && *force) sscanf(force, "%d,%d,%d", &nf, &u, &wv);
     if (epi == EPI_SWIGLU && (nf % 2)) nf = 2;

@@ -24,7 +24,8 @@ GEMM_SHAPES = [(1, 256, 256), (7, 768, 256), (16, 1376, 256), (33, 512, 688),
                (512, 22016, 256), (512, 12288, 256),  # one round of 192 x 256, 192 x 128 tiles
                (4, 73728, 256), (3, 36864, 320),    # LM-head-wide: 8 and 4 row tiles, 2 waves
                (9, 5120, 256), (5, 24576, 192),     # o/down wider than the CUs; 4-tile gate/up
-               (8, 4096, 1024)]                     # sixteen waves (o projection rule)
+               (8, 4096, 1024),                     # sixteen waves (o projection rule)
+               (3, 12288, 512)]                     # three row tiles, one workgroup per CU
 
 
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
