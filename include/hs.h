@@ -102,7 +102,10 @@ typedef struct {
 typedef enum {
   HS_W_EMBED = 0,      /* [vocab][hidden] */
   HS_W_ATTN_NORM = 1,  /* [hidden] RMSNorm gain before attention */
-  HS_W_QKV = 2,        /* [(n_heads + 2 n_kv_heads) head_dim][hidden]: q, k, v rows */
+  HS_W_QKV = 2,        /* [(n_heads + 2 n_kv_heads) head_dim][hidden]: q, k, v rows;
+                          inside each q and k head the two RoPE halves are
+                          interleaved in groups of 16 rows (rows 16j..16j+15 of
+                          the first half, then the same rows of the second) */
   HS_W_O = 3,          /* [hidden][n_heads head_dim] */
   HS_W_FFN_NORM = 4,   /* [hidden] RMSNorm gain before the FFN */
   HS_W_GATEUP = 5,     /* [2 ffn][hidden]: gate and up rows interleaved in
@@ -363,8 +366,9 @@ hs_status hs_kv_blob_describe(const void* host_blob, uint64_t avail,
  * Measurement. When timing is on, the stage's kernel launches are bracketed
  * by HIP events on their stream: every launch, or only those of the launch
  * sites named by hs_stage_set_timing_sites (a comma-separated list of
- * "embed", "attn_norm", "qkv", "rope_kv", "attn", "o_proj", "ffn_norm",
- * "gate_up", "down", "final_norm", "lm_head", "argmax", "kv_copy"; NULL or
+ * "embed", "attn_norm", "qkv" (the QKV projection with RoPE and the KV
+ * append), "attn", "o_proj", "ffn_norm", "gate_up", "down", "final_norm",
+ * "lm_head", "argmax", "kv_copy"; NULL or
  * "" = every site). Events between back-to-back kernels cost time of their
  * own, so timing a few sites disturbs a step less than timing all of them.
  * hs_stage_read_timing waits for the stage, then reports per (kernel, launch

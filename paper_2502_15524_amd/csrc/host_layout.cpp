@@ -219,6 +219,16 @@ extern "C" hs_status hs_weight_layout(const hs_model_cfg* cfg, int32_t rb, int32
   }
 }
 
+namespace {
+// Stored row of row i of a q or k projection with heads of d rows: inside a
+// head, row 16 j + r of the first half goes to 32 j + r and its RoPE partner
+// (the same row of the second half) to 32 j + 16 + r.
+uint64_t qk_row(uint64_t i, uint64_t d) {
+  const uint64_t h = i / d, r = i % d, half = d / 2;
+  return h * d + ((r % half) / 16) * 32 + (r / half) * 16 + r % 16;
+}
+}  // namespace
+
 extern "C" hs_status hs_image_put(const hs_model_cfg* cfg, int32_t rb, int32_t re, int32_t layer,
                                   int32_t src_kind, const uint16_t* src, uint64_t n_elems,
                                   void* image) {
@@ -262,8 +272,10 @@ extern "C" hs_status hs_image_put(const hs_model_cfg* cfg, int32_t rb, int32_t r
         return tile(L.lm_head, V, V, H, [](uint64_t i) { return i; });
       case HS_SRC_ATTN_NORM: return copy_rows(ls->attn_norm, 1, H);
       case HS_SRC_FFN_NORM: return copy_rows(ls->ffn_norm, 1, H);
-      case HS_SRC_WQ: return tile(ls->qkv, NQKV, QD, H, [](uint64_t i) { return i; });
-      case HS_SRC_WK: return tile(ls->qkv, NQKV, KD, H, [&](uint64_t i) { return QD + i; });
+      // q and k heads: the two RoPE halves interleaved in groups of 16 rows
+      case HS_SRC_WQ: return tile(ls->qkv, NQKV, QD, H, [&](uint64_t i) { return qk_row(i, D); });
+      case HS_SRC_WK:
+        return tile(ls->qkv, NQKV, KD, H, [&](uint64_t i) { return QD + qk_row(i, D); });
       case HS_SRC_WV: return tile(ls->qkv, NQKV, KD, H, [&](uint64_t i) { return QD + KD + i; });
       case HS_SRC_WO: return tile(ls->o, H, H, QD, [](uint64_t i) { return i; });
       case HS_SRC_WDOWN: return tile(ls->down, H, H, F, [](uint64_t i) { return i; });

@@ -68,6 +68,16 @@ __device__ __forceinline__ float silu_f(float g) {
   return g / (1.0f + fast_exp2(-g * 1.4426950408889634f));
 }
 
+// Rotate-half RoPE of one pair: x1 at index i of a head's first half, x2 at
+// i + D/2, angle with cosine c and sine s. Every kernel that rotates uses
+// these two (with explicit fused multiply-adds), so they all round alike.
+__device__ __forceinline__ float rope_first(float x1, float x2, float c, float s) {
+  return fmaf(x1, c, -(x2 * s));
+}
+__device__ __forceinline__ float rope_second(float x1, float x2, float c, float s) {
+  return fmaf(x2, c, x1 * s);
+}
+
 template <typename T>
 __device__ __forceinline__ T wave_sum(T v) {
 #pragma unroll

@@ -15,7 +15,9 @@ enum Epi : int {
   EPI_STORE = 0,   // Y = bf16(acc)
   EPI_RESID = 1,   // Y = bf16(R + acc); R may alias Y
   EPI_SWIGLU = 2,  // W rows interleave 16 gate / 16 up rows; Y[m][f] = bf16(silu(g) * u), width N/2
-  EPI_F32 = 3      // Y = acc as float32
+  EPI_F32 = 3,     // Y = acc as float32
+  EPI_QKV_ROPE = 4  // QKV projection: Y as EPI_STORE with q and k rotated (RoPE), k and v
+                    // also appended to the paged KV pool (fields rope_* below)
 };
 
 struct GemmArgs {
@@ -33,6 +35,20 @@ struct GemmArgs {
   // Optional RMSNorm of the rows of X with this gain (M <= 16, K % 64 == 0):
   // the product is then of rmsnorm(X) * gain, X being the raw rows.
   const bf16_t* norm_gain = nullptr; float norm_eps = 0.f;
+  // QKV projection with head-interleaved q and k rows: when rope_q_cols +
+  // rope_kv_cols > 0, the first rope_q_cols (q heads) and next rope_kv_cols (k
+  // heads) rows of W are stored per head as 32-row groups, 16 rows of the
+  // head's first half followed by the matching 16 rows of its second half
+  // (RoPE partners), so that a 32-row output pair holds both partners. Every
+  // store puts the columns back in head order. EPI_QKV_ROPE additionally
+  // rotates q and k (rotate-half RoPE at pos[m], tables [max_pos][D/2]) and
+  // writes k and v to token m's slot of the pool [blocks][2][n_kv][16][D]
+  // (slot < 0: no append); the v rows (the last rope_kv_cols) keep their order.
+  int rope_q_cols = 0, rope_kv_cols = 0, rope_d = 0;
+  const int32_t* rope_pos = nullptr; const int32_t* rope_slot = nullptr;
+  const float* rope_cos = nullptr; const float* rope_sin = nullptr;
+  int rope_max_pos = 0;
+  bf16_t* rope_pool = nullptr;
 };
 
 // Describes what was launched (for timing).

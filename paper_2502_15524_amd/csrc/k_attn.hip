@@ -321,11 +321,11 @@ __device__ __forceinline__ pack8 rope_chunk(const pack8& x, bool first, const fl
     const float o0 = lo_bf(x.w[e]), o1 = hi_bf(x.w[e]), p0 = lo_bf(pw), p1 = hi_bf(pw);
     float y0, y1;
     if (first) {
-      y0 = o0 * cs[2 * e] - p0 * sn[2 * e];
-      y1 = o1 * cs[2 * e + 1] - p1 * sn[2 * e + 1];
+      y0 = rope_first(o0, p0, cs[2 * e], sn[2 * e]);
+      y1 = rope_first(o1, p1, cs[2 * e + 1], sn[2 * e + 1]);
     } else {
-      y0 = o0 * cs[2 * e] + p0 * sn[2 * e];
-      y1 = o1 * cs[2 * e + 1] + p1 * sn[2 * e + 1];
+      y0 = rope_second(p0, o0, cs[2 * e], sn[2 * e]);
+      y1 = rope_second(p1, o1, cs[2 * e + 1], sn[2 * e + 1]);
     }
     y.w[e] = pack2bf(y0, y1);
   }
@@ -563,8 +563,8 @@ __device__ __forceinline__ void rope_pair(pack8& x1, pack8& x2, const float* cs,
     const float a0 = lo_bf(x1.w[e]), a1 = hi_bf(x1.w[e]);
     const float b0 = lo_bf(x2.w[e]), b1 = hi_bf(x2.w[e]);
     const float c0 = cs[2 * e], c1 = cs[2 * e + 1], s0 = sn[2 * e], s1 = sn[2 * e + 1];
-    x1.w[e] = pack2bf(a0 * c0 - b0 * s0, a1 * c1 - b1 * s1);
-    x2.w[e] = pack2bf(b0 * c0 + a0 * s0, b1 * c1 + a1 * s1);
+    x1.w[e] = pack2bf(rope_first(a0, b0, c0, s0), rope_first(a1, b1, c1, s1));
+    x2.w[e] = pack2bf(rope_second(a0, b0, c0, s0), rope_second(a1, b1, c1, s1));
   }
 }
 

@@ -33,9 +33,19 @@ namespace hs {
 
 // ---------------------------------------------------------------- epilogue
 
+// Output column (head order) of column n of a QKV projection whose q and k
+// rows are stored head-interleaved: inside a head, the 32-row group p holds
+// rows 16p .. 16p + 15 of the first half, then the same rows of the second.
+__device__ __forceinline__ int qk_col(const GemmArgs& a, int n) {
+  if (n >= a.rope_q_cols + a.rope_kv_cols) return n;
+  const int d = n & (a.rope_d - 1);
+  return (n - d) + ((d >> 4) & 1) * (a.rope_d >> 1) + (d >> 5) * 16 + (d & 15);
+}
+
 template <int EPI>
 __device__ __forceinline__ void store4(const GemmArgs& a, int m, int f, const f32x4_v& v) {
   if (m >= a.M || f >= a.N) return;
+  if constexpr (EPI == EPI_STORE) f = qk_col(a, f);
   if constexpr (EPI == EPI_F32) {
     float4 o = make_float4(v[0], v[1], v[2], v[3]);
     *reinterpret_cast<float4*>(static_cast<float*>(a.Y) + (int64_t)m * a.ldy + f) = o;
@@ -61,6 +71,65 @@ __device__ __forceinline__ void store_swiglu(const GemmArgs& a, int m, int f, co
   o.x = pack2bf(silu_f(g[0]) * u[0], silu_f(g[1]) * u[1]);
   o.y = pack2bf(silu_f(g[2]) * u[2], silu_f(g[3]) * u[3]);
   *reinterpret_cast<uint2*>(static_cast<bf16_t*>(a.Y) + (int64_t)m * a.ldy + f) = o;
+}
+
+// QKV projection with RoPE and KV append. n is the (stored-order) column of
+// x1's first value, a multiple of 4 inside the first 16 rows of a 32-row
+// pair; x2 holds the pair's other 16 rows. In the q and k heads these are
+// RoPE partners (rotation index i and i + D/2); in the v heads two adjacent
+// 16-column groups. Values are rounded to bf16 before the rotation, as a
+// separate rotation pass reading the stored projection would see them.
+
+// rotation index of column n (< rope_q_cols + rope_kv_cols) and its table offset
+__device__ __forceinline__ int64_t rope_tab_off(const GemmArgs& a, int pos, int n) {
+  const int d = n & (a.rope_d - 1);
+  return (int64_t)pos * (a.rope_d >> 1) + (d >> 5) * 16 + (d & 15);
+}
+
+// cv, sv: cos and sin at rope_tab_off(a, pos, n) (unused for v columns)
+__device__ __forceinline__ void store_qkv_rope(const GemmArgs& a, int m, int slot, int n,
+                                               const f32x4_v& x1, const f32x4_v& x2,
+                                               const float4& cv, const float4& sv) {
+  if (m >= a.M || n >= a.N) return;
+  const int D = a.rope_d, half = D >> 1;
+  uint2 o1, o2;
+  o1.x = pack2bf(x1[0], x1[1]);
+  o1.y = pack2bf(x1[2], x1[3]);
+  o2.x = pack2bf(x2[0], x2[1]);
+  o2.y = pack2bf(x2[2], x2[3]);
+  int c1, c2;  // output columns of x1 and x2
+  if (n < a.rope_q_cols + a.rope_kv_cols) {
+    const int d = n & (D - 1);
+    c1 = (n - d) + (d >> 5) * 16 + (d & 15);
+    c2 = c1 + half;
+    const float cc[4] = {cv.x, cv.y, cv.z, cv.w}, ss[4] = {sv.x, sv.y, sv.z, sv.w};
+    const float p1[4] = {lo_bf(o1.x), hi_bf(o1.x), lo_bf(o1.y), hi_bf(o1.y)};
+    const float p2[4] = {lo_bf(o2.x), hi_bf(o2.x), lo_bf(o2.y), hi_bf(o2.y)};
+    float y1[4], y2[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      y1[e] = rope_first(p1[e], p2[e], cc[e], ss[e]);
+      y2[e] = rope_second(p1[e], p2[e], cc[e], ss[e]);
+    }
+    o1 = make_uint2(pack2bf(y1[0], y1[1]), pack2bf(y1[2], y1[3]));
+    o2 = make_uint2(pack2bf(y2[0], y2[1]), pack2bf(y2[2], y2[3]));
+  } else {
+    c1 = n;
+    c2 = n + 16;
+  }
+  bf16_t* row = static_cast<bf16_t*>(a.Y) + (int64_t)m * a.ldy;
+  *reinterpret_cast<uint2*>(row + c1) = o1;
+  *reinterpret_cast<uint2*>(row + c2) = o2;
+  if (slot >= 0 && n >= a.rope_q_cols) {
+    // k head kh -> pool part 0, v head kh -> part 1 of the token's block
+    const int n_kv = a.rope_kv_cols / D;
+    const int kv = c1 - a.rope_q_cols;  // column inside the k (then v) heads
+    const int kh = kv / D;              // 0 .. 2 n_kv - 1: k heads, then v heads
+    bf16_t* dst = a.rope_pool + (int64_t)(slot >> 4) * 2 * n_kv * 16 * D +
+                  ((int64_t)kh * 16 + (slot & 15)) * D + (kv - kh * D);
+    *reinterpret_cast<uint2*>(dst) = o1;
+    *reinterpret_cast<uint2*>(dst + (c2 - c1)) = o2;
+  }
 }
 
 // ------------------------------------ tiled, buffer loads into an LDS ring
@@ -228,7 +297,8 @@ void gemm_ring(GemmArgs a, GemmSched sc) {
   using T = RTile<BN, BM, BK, NS>;
   constexpr int CPR = T::CPR, RPI = T::RPI, WN = T::WN, WM = T::WM, TN = T::TN, TM = T::TM;
   constexpr int LPS = T::LPS;
-  static_assert(EPI != EPI_SWIGLU || (WN % 32) == 0, "SwiGLU needs gate/up tile pairs");
+  static_assert((EPI != EPI_SWIGLU && EPI != EPI_QKV_ROPE) || (WN % 32) == 0,
+                "SwiGLU and RoPE need 32-row pairs");
   __shared__ __attribute__((aligned(1024))) char smem[NS * T::STAGE];
   __shared__ int s_last;
 
@@ -255,7 +325,42 @@ void gemm_ring(GemmArgs a, GemmSched sc) {
   f32x4_v acc[TN][TM];
 
   // acc = sum over k steps [k0, k1) of tile (n0, m0)
-  auto mainloop = [&](int n0, int m0, int k0, int k1) {
+  // QKV projection with RoPE, data-parallel tiles: the tile's token
+  // positions and slots, and its cos/sin rows when they fit in registers, are
+  // requested right after the main loop's first operand loads, so their round
+  // trips overlap the pipeline start instead of delaying the epilogue. (Extra
+  // loads only make the vmcnt waits of the ring stricter: loads complete in
+  // order.)
+  constexpr bool ROPE_PRE = EPI == EPI_QKV_ROPE && !SK;
+  constexpr bool ROPE_TAB = ROPE_PRE && TN * TM <= 32;
+  constexpr int RJ = ROPE_PRE ? TM : 1, RJT = ROPE_TAB ? TM : 1, RI = ROPE_TAB ? TN / 2 : 1;
+  int r_pos[RJ], r_slot[RJ];
+  float4 r_cos[RJT][RI], r_sin[RJT][RI];
+  auto rope_fetch = [&](int n0, int m0) {
+    if constexpr (ROPE_PRE) {
+#pragma unroll
+      for (int j = 0; j < TM; ++j) {
+        const int m = m0 + wm * WM + j * 16 + fr;
+        const bool in = m < a.M;
+        r_pos[j] = in ? a.rope_pos[m] : 0;
+        r_slot[j] = in ? a.rope_slot[m] : -1;
+      }
+      if constexpr (ROPE_TAB) {
+        const int qk = a.rope_q_cols + a.rope_kv_cols;
+#pragma unroll
+        for (int j = 0; j < TM; ++j)
+#pragma unroll
+          for (int ip = 0; ip < TN / 2; ++ip) {
+            const int n = n0 + wn * WN + ip * 32 + g * 4;
+            const int64_t o = rope_tab_off(a, r_pos[j], n < qk ? n : 0);
+            r_cos[j][ip] = *reinterpret_cast<const float4*>(a.rope_cos + o);
+            r_sin[j][ip] = *reinterpret_cast<const float4*>(a.rope_sin + o);
+          }
+      }
+    }
+  };
+
+  auto mainloop = [&](int n0, int m0, int k0, int k1, auto&& after_issue) {
 #pragma unroll
     for (int i = 0; i < TN; ++i)
 #pragma unroll
@@ -289,6 +394,7 @@ void gemm_ring(GemmArgs a, GemmSched sc) {
 #pragma unroll
         for (int q = 0; q < LPS; ++q) issue_one(s, k0 + s, q);
       }
+    after_issue();
     if (n >= NS - 1) wait_vm<(NS - 2) * LPS>();
     else wait_vm<0>();
     wg_barrier();
@@ -320,6 +426,31 @@ void gemm_ring(GemmArgs a, GemmSched sc) {
 #pragma unroll
         for (int i = 0; i < TN; i += 2)
           store_swiglu(a, m, (n0 + wn * WN + i * 16) / 2 + fq, acc[i][j], acc[i + 1][j]);
+      } else if constexpr (EPI == EPI_QKV_ROPE) {
+        int pos, slot;
+        if constexpr (ROPE_PRE) {
+          pos = r_pos[j];
+          slot = r_slot[j];
+        } else {
+          const bool in = m < a.M;
+          pos = in ? a.rope_pos[m] : 0;
+          slot = in ? a.rope_slot[m] : -1;
+        }
+        const int qk = a.rope_q_cols + a.rope_kv_cols;
+#pragma unroll
+        for (int i = 0; i < TN; i += 2) {
+          const int n = n0 + wn * WN + i * 16 + fq;
+          float4 cv, sv;
+          if constexpr (ROPE_TAB) {
+            cv = r_cos[j][i / 2];
+            sv = r_sin[j][i / 2];
+          } else {
+            const int64_t o = rope_tab_off(a, pos, n < qk ? n : 0);
+            cv = *reinterpret_cast<const float4*>(a.rope_cos + o);
+            sv = *reinterpret_cast<const float4*>(a.rope_sin + o);
+          }
+          store_qkv_rope(a, m, slot, n, acc[i][j], acc[i + 1][j], cv, sv);
+        }
       } else {
 #pragma unroll
         for (int i = 0; i < TN; ++i) store4<EPI>(a, m, n0 + wn * WN + i * 16 + fq, acc[i][j]);
@@ -330,7 +461,7 @@ void gemm_ring(GemmArgs a, GemmSched sc) {
   if constexpr (!SK) {
     int nt, mt;
     tile_coords(sc, l, nt, mt);
-    mainloop(nt * BN, mt * BM, 0, sc.nk);
+    mainloop(nt * BN, mt * BM, 0, sc.nk, [&] { rope_fetch(nt * BN, mt * BM); });
     epilogue(nt * BN, mt * BM);
   } else {
 
@@ -354,7 +485,7 @@ void gemm_ring(GemmArgs a, GemmSched sc) {
     const int k1 = (int)min<int64_t>(sc.nk, k0 + (end - it));
     int nt, mt;
     tile_coords(sc, t, nt, mt);
-    mainloop(nt * BN, mt * BM, k0, k1);
+    mainloop(nt * BN, mt * BM, k0, k1, [] {});
     if (k0 > 0 || k1 < sc.nk) {
       const int slot = it == beg ? 0 : 1;
       const int mine = (2 * l + slot) * TILE_F * 4;
@@ -667,6 +798,7 @@ hipError_t dispatch_ring(const GemmArgs& a, int epi, const GemmSched& sc, int gr
     case EPI_RESID: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_RESID>), dim3(grid), dim3(256), 0, s, a, sc); break;
     case EPI_SWIGLU: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_SWIGLU>), dim3(grid), dim3(256), 0, s, a, sc); break;
     case EPI_F32: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_F32>), dim3(grid), dim3(256), 0, s, a, sc); break;
+    case EPI_QKV_ROPE: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_QKV_ROPE>), dim3(grid), dim3(256), 0, s, a, sc); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -711,13 +843,26 @@ int device_cus() {
   return cus[dev];
 }
 
-const char* kEpiName[4] = {"store", "resid", "swiglu", "f32"};
+const char* kEpiName[5] = {"store", "resid", "swiglu", "f32", "qkv_rope"};
 
 }  // namespace
 
 hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info) {
   if (a.M <= 0 || a.N <= 0 || a.K <= 0) return hipErrorInvalidValue;
-  if (epi < 0 || epi > 3) return hipErrorInvalidValue;
+  if (epi < 0 || epi > 4) return hipErrorInvalidValue;
+  // head-interleaved q/k rows: whole heads of 64 or 128, then as many v columns as k
+  if (a.rope_q_cols || a.rope_kv_cols) {
+    const int d = a.rope_d;
+    if ((d != 64 && d != 128) || a.rope_q_cols <= 0 || a.rope_kv_cols <= 0 ||
+        (a.rope_q_cols % d) || (a.rope_kv_cols % d) || a.rope_q_cols + 2 * a.rope_kv_cols != a.N)
+      return hipErrorInvalidValue;
+  }
+  if (epi == EPI_QKV_ROPE &&
+      (!a.rope_q_cols || !a.rope_pos || !a.rope_slot || !a.rope_cos || !a.rope_sin ||
+       !a.rope_pool || a.rope_max_pos <= 0 || (a.ldy % 8) ||
+       ((uintptr_t)a.rope_cos & 15) || ((uintptr_t)a.rope_sin & 15) ||
+       ((uintptr_t)a.rope_pool & 15)))
+    return hipErrorInvalidValue;
   const int64_t kp = (a.K + 63) / 64 * 64;
   if ((a.K % 8) || (a.N % 16) || (a.ldx % 8) || (a.ldy % 4)) return hipErrorInvalidValue;
   if ((a.K % 64) && a.ldx < kp) return hipErrorInvalidValue;
@@ -738,6 +883,9 @@ hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info) {
   const double bytes = 2.0 * ((double)a.M * a.K + (double)a.N * a.K) + out_bytes;
   hipError_t e;
   if (a.M <= 64) {
+    // a QKV projection with RoPE runs as a plain (head-order) store followed
+    // by the rotation pass
+    const int pe = epi == EPI_QKV_ROPE ? EPI_STORE : epi;
     const int mch = (a.M + 15) / 16;
     // Rows per workgroup (16 NF), 64-k slabs per load group (U) and waves per
     // workgroup (WV) for one token chunk, from a sweep on MI355X over the
@@ -756,38 +904,44 @@ hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info) {
     static const char* force = getenv("HS_SKINNY_CFG");
     const int cus = device_cus();
     int nf = 1, u = 1, wv = 4;
-    if (epi == EPI_F32) {
+    if (pe == EPI_F32) {
       nf = 2, wv = 2;
       while (nf < 8 && a.N / (16 * nf) > 1100) nf *= 2;
-    } else if (epi == EPI_SWIGLU) {
+    } else if (pe == EPI_SWIGLU) {
       nf = (a.N / 64 >= cus + cus / 2) ? 4 : 2;
-    } else if (epi == EPI_RESID) {
+    } else if (pe == EPI_RESID) {
       wv = 8;
       if (a.N / 16 > cus) nf = a.M > 4 ? 2 : 1;
       else if (a.K <= 4096) wv = 16;  // 4096 x 4096 o projection: 9.4 -> 8.2 us at 8 tokens
       else u = a.M <= 8 ? 2 : 1;
-    } else if (epi == EPI_STORE) {
+    } else if (pe == EPI_STORE) {
       nf = 2, wv = a.N <= 8192 ? 8 : 4;
       // three row tiles when that gives one workgroup per CU (7B QKV: 256 x
       // 48 rows; 21.5 -> 19.5 us)
       if (a.N % 48 == 0 && a.N / 48 <= cus && a.N / 48 > cus * 3 / 4) nf = 3, wv = 16;
     }
     if (force && *force) sscanf(force, "%d,%d,%d", &nf, &u, &wv);
-    if (epi == EPI_SWIGLU && (nf % 2)) nf = 2;
+    if (pe == EPI_SWIGLU && (nf % 2)) nf = 2;
     if (mch == 1) {
-      e = dispatch_skinny1(a, epi, nf, u, wv, s);
-    } else if (epi == EPI_SWIGLU) {
+      e = dispatch_skinny1(a, pe, nf, u, wv, s);
+    } else if (pe == EPI_SWIGLU) {
       switch (mch) {
-        case 2: e = dispatch_epi_skinny<2, 2, 2, 4>(a, epi, s); break;
-        case 3: e = dispatch_epi_skinny<2, 3, 1, 4>(a, epi, s); break;
-        default: e = dispatch_epi_skinny<2, 4, 1, 4>(a, epi, s); break;
+        case 2: e = dispatch_epi_skinny<2, 2, 2, 4>(a, pe, s); break;
+        case 3: e = dispatch_epi_skinny<2, 3, 1, 4>(a, pe, s); break;
+        default: e = dispatch_epi_skinny<2, 4, 1, 4>(a, pe, s); break;
       }
     } else {
       switch (mch) {
-        case 2: e = dispatch_epi_skinny<1, 2, 2, 4>(a, epi, s); break;
-        case 3: e = dispatch_epi_skinny<1, 3, 2, 4>(a, epi, s); break;
-        default: e = dispatch_epi_skinny<1, 4, 1, 4>(a, epi, s); break;
+        case 2: e = dispatch_epi_skinny<1, 2, 2, 4>(a, pe, s); break;
+        case 3: e = dispatch_epi_skinny<1, 3, 2, 4>(a, pe, s); break;
+        default: e = dispatch_epi_skinny<1, 4, 1, 4>(a, pe, s); break;
       }
+    }
+    if (e == hipSuccess && epi == EPI_QKV_ROPE) {
+      RopeKvArgs r{static_cast<bf16_t*>(a.Y), a.ldy, a.rope_pos, a.rope_slot, a.rope_cos,
+                   a.rope_sin, a.rope_pool, a.M, a.rope_q_cols / a.rope_d,
+                   a.rope_kv_cols / a.rope_d, a.rope_d, a.rope_max_pos};
+      e = rope_kv(r, s, nullptr);
     }
     snprintf(name, sizeof name, "gemm_skinny_%s%s", a.norm_gain ? "norm_" : "", kEpiName[epi]);
   } else {

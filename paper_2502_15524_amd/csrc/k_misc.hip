@@ -31,7 +31,9 @@ hipError_t embed(const int32_t* tok, const bf16_t* E, int vocab, int hidden, int
 
 // ------------------------------------------------------------------ RMSNorm
 
-// One workgroup per row; each thread keeps up to 4 chunks of 8 values.
+// One workgroup per row; each thread keeps up to 4 chunks of 8 values and
+// loads the gain's chunks together with the row's (one memory round trip per
+// row: the gain does not wait for the reduction).
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const bf16_t* x, int64_t ldx,
                                                       const int32_t* rows, int hidden,
                                                       const bf16_t* gain, float eps, bf16_t* out,
@@ -41,20 +43,25 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const bf16_t* x, int64_t l
   const int src = rows ? rows[r] : r;
   const bf16_t* xr = x + (int64_t)src * ldx;
   const int chunks = hidden / 8;
-  float v[4][8];
-  float ss = 0.f;
+  pack8 xv[4], gv[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int c = threadIdx.x + i * 256;
     if (c < chunks) {
-      const pack8 p = ld16(xr + c * 8);
+      xv[i] = ld16(xr + c * 8);
+      gv[i] = ld16(gain + c * 8);
+    }
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if (threadIdx.x + i * 256 < chunks) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        v[i][2 * e] = lo_bf(p.w[e]);
-        v[i][2 * e + 1] = hi_bf(p.w[e]);
+        const float lo = lo_bf(xv[i].w[e]), hi = hi_bf(xv[i].w[e]);
+        ss += lo * lo;
+        ss += hi * hi;
       }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) ss += v[i][e] * v[i][e];
     }
   }
   ss = wave_sum(ss);
@@ -67,11 +74,11 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const bf16_t* x, int64_t l
   for (int i = 0; i < 4; ++i) {
     const int c = threadIdx.x + i * 256;
     if (c < chunks) {
-      const pack8 gp = ld16(gain + c * 8);
       pack8 o;
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        o.w[e] = pack2bf(v[i][2 * e] * inv * lo_bf(gp.w[e]), v[i][2 * e + 1] * inv * hi_bf(gp.w[e]));
+        o.w[e] = pack2bf(lo_bf(xv[i].w[e]) * inv * lo_bf(gv[i].w[e]),
+                         hi_bf(xv[i].w[e]) * inv * hi_bf(gv[i].w[e]));
       st16(orow + c * 8, o);
     }
   }
@@ -122,8 +129,8 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(RopeKvArgs a) {
     float y1[4], y2[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      y1[e] = x1[e] * cc[e] - x2[e] * ss[e];
-      y2[e] = x2[e] * cc[e] + x1[e] * ss[e];
+      y1[e] = rope_first(x1[e], x2[e], cc[e], ss[e]);
+      y2[e] = rope_second(x1[e], x2[e], cc[e], ss[e]);
     }
     const uint2 o1 = make_uint2(pack2bf(y1[0], y1[1]), pack2bf(y1[2], y1[3]));
     const uint2 o2 = make_uint2(pack2bf(y2[0], y2[1]), pack2bf(y2[2], y2[3]));

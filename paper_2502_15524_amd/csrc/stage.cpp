@@ -411,18 +411,20 @@ hs_status layer_forward(hs_stage* st, int l, bf16_t* x, const LayerCall& c, hipS
                      ? gemm_args(st, x, H, W(st, ls.qkv), st->w_qkv, NQKV, nullptr, 0, c.T, NQKV, H)
                      : gemm_args(st, st->w_u, H, W(st, ls.qkv), st->w_qkv, NQKV, nullptr, 0, c.T, NQKV, H);
     if (fuse_norm) g.norm_gain = W(st, ls.attn_norm), g.norm_eps = m.rms_eps;
-    return gemm(g, EPI_STORE, s, i);
+    // the image stores q and k heads with their RoPE halves interleaved
+    g.rope_q_cols = QD;
+    g.rope_kv_cols = m.n_kv_heads * D;
+    g.rope_d = D;
+    if (c.decode) return gemm(g, EPI_STORE, s, i);  // the attention kernel rotates and appends
+    g.rope_pos = c.pos;
+    g.rope_slot = c.slot;
+    g.rope_cos = st->d_cos;
+    g.rope_sin = st->d_sin;
+    g.rope_max_pos = st->opts.max_ctx;
+    g.rope_pool = pool(st, l);
+    return gemm(g, EPI_QKV_ROPE, s, i);
   });
   if (r != HS_OK) return r;
-  // a decode step rotates and appends inside the attention kernel
-  if (!c.decode) {
-    r = run(st, s, "rope_kv", [&](LaunchInfo* i) {
-      RopeKvArgs a{st->w_qkv, NQKV, c.pos, c.slot, st->d_cos, st->d_sin, pool(st, l),
-                   c.T, m.n_heads, m.n_kv_heads, D, st->opts.max_ctx};
-      return rope_kv(a, s, i);
-    });
-    if (r != HS_OK) return r;
-  }
   if (!c.decode) {
     r = run(st, s, "attn", [&](LaunchInfo* i) {
       AttnPrefillArgs a{st->w_qkv, NQKV, st->w_attn, QD, c.cu, c.tiles, c.n_tiles,

@@ -381,7 +381,7 @@ def test_timing_sites_filter(env):
     h_all = _hidden_prefill_full(st, env["prompt"], seq_id=1)
     all_stats = hs.hs_stage_read_timing(st.h)
     sites = {s["site"] for s in all_stats}
-    assert {"embed", "attn_norm", "qkv", "rope_kv", "attn", "o_proj", "ffn_norm", "gate_up",
+    assert {"embed", "attn_norm", "qkv", "attn", "o_proj", "ffn_norm", "gate_up",
             "down", "final_norm", "lm_head", "argmax"} <= sites
     hs.hs_stage_set_timing_sites(st.h, "qkv, down")
     h_two = _hidden_prefill_full(st, env["prompt"], seq_id=2)

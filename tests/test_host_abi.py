@@ -91,8 +91,18 @@ def test_image_put_places_tensors():
 
     qkv = tensor(hs.HS_W_QKV)
     wq = gen.to_bf16_bits(gen.weight_f32(cfg, 1, "wq"))
+    wk = gen.to_bf16_bits(gen.weight_f32(cfg, 1, "wk"))
     wv = gen.to_bf16_bits(gen.weight_f32(cfg, 1, "wv"))
-    assert np.array_equal(qkv[:256], wq) and np.array_equal(qkv[512:], wv)
+    # q and k heads (d = 64): rows 16j + r of the first half at 32j + r, their
+    # RoPE partners (row + 32) at 32j + 16 + r; v rows in order
+    d = cfg.head_dim
+    for h in range(cfg.n_heads):
+        for i in range(d):
+            j, r, second = (i % (d // 2)) // 16, i % 16, i // (d // 2)
+            stored = h * d + 32 * j + 16 * second + r
+            assert np.array_equal(qkv[stored], wq[h * d + i])
+            assert np.array_equal(qkv[256 + stored], wk[h * d + i])
+    assert np.array_equal(qkv[512:], wv)
     gu = tensor(hs.HS_W_GATEUP)
     g = gen.to_bf16_bits(gen.weight_f32(cfg, 1, "wgate"))
     u = gen.to_bf16_bits(gen.weight_f32(cfg, 1, "wup"))
