@@ -180,13 +180,15 @@ def _paged_case(lens, nh, nkv, d, seed):
     return q, pool, table, ks, vs
 
 
-def test_attn_decode_batch_invariant():
-    """A sequence's output has the same bits alone and inside a ragged
-    16-sequence batch."""
+@pytest.mark.parametrize("lens,nh,nkv,d", [
+    ([2100] + [int(x) for x in np.random.default_rng(3).integers(900, 2000, 15)], 32, 8, 128),
+    ([600, 2000, 17, 641, 640], 32, 32, 128),    # one query head per kv head
+    ([2000, 600, 17, 641, 640], 32, 32, 128),
+    ([641, 5, 1300, 639], 4, 4, 64)])
+def test_attn_decode_batch_invariant(lens, nh, nkv, d):
+    """A sequence's output has the same bits alone and inside a ragged batch."""
     torch = G.torch()
     hs = _hs()
-    lens = [2100] + [int(x) for x in np.random.default_rng(3).integers(900, 2000, 15)]
-    nh, nkv, d = 32, 8, 128
     q, pool, table, _, _ = _paged_case(lens, nh, nkv, d, 77)
     dq = G.to_dev_bf16(q)
     dpool = G.to_dev_bf16(pool.reshape(-1))
@@ -207,7 +209,8 @@ def test_attn_decode_batch_invariant():
 @pytest.mark.parametrize("lens,nh,nkv,d", [
     ([1], 4, 4, 64), ([17, 300, 64, 65], 4, 4, 64), ([5, 130, 1100, 64, 2100], 32, 8, 128),
     ([512], 32, 32, 128), ([2, 129, 700], 8, 2, 128), ([1000, 33], 16, 4, 64),
-    ([300, 17, 129], 8, 4, 128)])   # two query heads per kv head
+    ([300, 17, 129], 8, 4, 128),    # two query heads per kv head
+    ([700, 641, 640, 1, 129], 8, 8, 128), ([1300, 639, 5, 641], 4, 4, 64)])
 def test_attn_decode(lens, nh, nkv, d):
     """One query per sequence (at position ctx - 1) over a paged cache, against
     the oracle's attention; a second call gives the same bits."""
@@ -237,7 +240,7 @@ def test_attn_decode(lens, nh, nkv, d):
 @pytest.mark.parametrize("lens,nh,nkv,d", [
     ([1], 4, 4, 64), ([17, 300, 64, 65], 4, 4, 64), ([5, 130, 1100, 64, 2100], 32, 8, 128),
     ([512], 32, 32, 128), ([1000, 33, 16], 16, 4, 64), ([80, 64, 63, 2], 8, 2, 128),
-    ([300, 17, 129], 8, 4, 128)])
+    ([300, 17, 129], 8, 4, 128), ([650, 640, 3, 576], 8, 8, 128), ([641, 600, 64], 4, 4, 64)])
 def test_attn_decode_rope(lens, nh, nkv, d):
     """Decode attention with the step's RoPE and cache append folded in. The
     last position of each sequence is the new token, given before RoPE in a
