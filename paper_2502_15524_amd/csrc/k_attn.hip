@@ -31,9 +31,17 @@ namespace hs {
 
 typedef short s16x4_v __attribute__((ext_vector_type(4)));
 
-template <int D, int NW>
-__global__ __launch_bounds__(64 * NW) void attn_prefill_kernel(AttnPrefillArgs a, float scale_log2) {
-  constexpr int NT = 64 * NW;   // threads
+// KS = 2 (key split, 8 waves on a 64-query tile): waves w and w + 4 own the
+// same 16 queries; the first takes the even key blocks, the second the odd
+// ones, each half of the workgroup staging its own block, and at the end the
+// second hands its running max, sum and output to the first through LDS
+// (a fixed merge order). Two waves per SIMD hide each block's serial chain
+// (score MFMAs, cross-lane max, exp2, P V MFMAs) when the tiles fill at most
+// one workgroup per CU.
+template <int D, int NW, int KS>
+__global__ __launch_bounds__(64 * NW * KS) void attn_prefill_kernel(AttnPrefillArgs a, float scale_log2) {
+  static_assert(KS == 1 || (KS == 2 && NW == 4), "key split: 2 x 4 waves");
+  constexpr int NT = 64 * NW;   // threads staging one key block
   constexpr int QT = 16 * NW;   // queries per workgroup
   constexpr int KB = 64;        // keys per block
   constexpr int LK = D + 8;     // padded K row in LDS
@@ -43,12 +51,22 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_kernel(AttnPrefillArgs a
   constexpr int KPP = NT / CPK; // key rows per load pass
   constexpr int PASS = KB / KPP;
   static_assert(KB % KPP == 0 && (KPP % 2) == 0, "load mapping");
-  __shared__ __attribute__((aligned(16))) bf16_t sK[KB * LK];
-  __shared__ __attribute__((aligned(16))) bf16_t sV[KB * LV];
+  __shared__ __attribute__((aligned(16))) bf16_t sKb[KS][KB * LK];
+  __shared__ __attribute__((aligned(16))) bf16_t sVb[KS][KB * LV];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int seq = a.tiles[2 * blockIdx.x], q0 = a.tiles[2 * blockIdx.x + 1];
-  const int h = blockIdx.y;
+  const int part = KS == 1 ? 0 : threadIdx.x / NT;  // key parity of this half
+  bf16_t* const sK = sKb[part];
+  bf16_t* const sV = sVb[part];
+  const int tid = threadIdx.x % NT, lane = tid & 63, wave = tid >> 6;
+  // Workgroup b runs on XCD b mod 8: the logical (tile, head) order puts the
+  // tiles of one head, which read the same keys and values, on one XCD (and
+  // its L2) instead of spreading them over all eight.
+  const int nwg = gridDim.x * gridDim.y;
+  int lwg = blockIdx.x + blockIdx.y * gridDim.x;
+  if ((nwg & 7) == 0) lwg = (lwg & 7) * (nwg >> 3) + (lwg >> 3);
+  const int tile = lwg % gridDim.x;
+  const int seq = a.tiles[2 * tile], q0 = a.tiles[2 * tile + 1];
+  const int h = lwg / gridDim.x;
   const int kh = h / (a.n_heads / a.n_kv_heads);
   const int base = a.cu[seq], len = a.cu[seq + 1] - base;
   const int fr = lane & 15, g = lane >> 4;
@@ -83,9 +101,10 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_kernel(AttnPrefillArgs a
       vreg[p] = key < len ? ld16(vbase + (int64_t)key * a.ld + lcol) : zero8();
     }
   };
-  fetch(0);
+  fetch(part);  // past the last block: zero rows, never multiplied
 
-  for (int kb = 0; kb < n_kb; ++kb) {
+  for (int kb0 = 0; kb0 < n_kb; kb0 += KS) {
+    const int kb = kb0 + part;
     const int k0 = kb * KB;
     __syncthreads();  // every wave is done with the previous block
 #pragma unroll
@@ -95,8 +114,8 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_kernel(AttnPrefillArgs a
       st16(&sV[key * LV + lcol], vreg[p]);
     }
     __syncthreads();
-    if (kb + 1 < n_kb) fetch(kb + 1);  // in flight during this block's MFMAs
-    if (k0 > qw0 + 15) continue;       // block entirely in this wave's future
+    if (kb0 + KS < n_kb) fetch(kb + KS);  // in flight during this block's MFMAs
+    if (kb >= n_kb || k0 > qw0 + 15) continue;  // no such block, or in this wave's future
 
     f32x4_v s[4];
 #pragma unroll
@@ -171,6 +190,27 @@ __global__ __launch_bounds__(64 * NW) void attn_prefill_kernel(AttnPrefillArgs a
     }
   }
 
+  if constexpr (KS == 2) {
+    // odd-block waves hand (max, sum, output) to the even-block waves, lane by lane
+    __shared__ float s_m[NW][64], s_l[NW][64];
+    __shared__ f32x4_v s_o[NW][D / 16][64];
+    __syncthreads();
+    if (part == 1) {
+      s_m[wave][lane] = m_run;
+      s_l[wave][lane] = l_run;
+#pragma unroll
+      for (int i = 0; i < D / 16; ++i) s_o[wave][i][lane] = o[i];
+    }
+    __syncthreads();
+    if (part == 1) return;
+    const float m1 = s_m[wave][lane], l1 = s_l[wave][lane];
+    const float m = fmaxf(m_run, m1);  // finite: the even half always has block 0
+    const float c0 = fast_exp2(m_run - m), c1 = fast_exp2(m1 - m);  // m1 = -inf gives 0
+    l_run = l_run * c0 + l1 * c1;
+#pragma unroll
+    for (int i = 0; i < D / 16; ++i) o[i] = o[i] * c0 + s_o[wave][i][lane] * c1;
+  }
+
   float l_tot = l_run + __shfl_xor(l_run, 16, 64);
   l_tot += __shfl_xor(l_tot, 32, 64);
   if (qrow >= len) return;
@@ -192,14 +232,29 @@ hipError_t attn_prefill(const AttnPrefillArgs& a, hipStream_t s, LaunchInfo* inf
     return hipErrorInvalidValue;
   const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)a.D));
   dim3 grid(a.n_tiles, a.n_heads);
+  // 4-wave tiles that fit one workgroup per CU take the key split (8 waves)
+  static int cus = 0;
+  if (!cus) {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
+      cus = n;
+    else
+      cus = 1;
+  }
+  const bool ks = a.waves == 4 && (int64_t)a.n_tiles * a.n_heads <= cus;
   if (a.D == 128 && a.waves == 8)
-    hipLaunchKernelGGL((attn_prefill_kernel<128, 8>), grid, dim3(512), 0, s, a, scale_log2);
+    hipLaunchKernelGGL((attn_prefill_kernel<128, 8, 1>), grid, dim3(512), 0, s, a, scale_log2);
+  else if (a.D == 128 && ks)
+    hipLaunchKernelGGL((attn_prefill_kernel<128, 4, 2>), grid, dim3(512), 0, s, a, scale_log2);
   else if (a.D == 128)
-    hipLaunchKernelGGL((attn_prefill_kernel<128, 4>), grid, dim3(256), 0, s, a, scale_log2);
+    hipLaunchKernelGGL((attn_prefill_kernel<128, 4, 1>), grid, dim3(256), 0, s, a, scale_log2);
   else if (a.waves == 8)
-    hipLaunchKernelGGL((attn_prefill_kernel<64, 8>), grid, dim3(512), 0, s, a, scale_log2);
+    hipLaunchKernelGGL((attn_prefill_kernel<64, 8, 1>), grid, dim3(512), 0, s, a, scale_log2);
+  else if (ks)
+    hipLaunchKernelGGL((attn_prefill_kernel<64, 4, 2>), grid, dim3(512), 0, s, a, scale_log2);
   else
-    hipLaunchKernelGGL((attn_prefill_kernel<64, 4>), grid, dim3(256), 0, s, a, scale_log2);
+    hipLaunchKernelGGL((attn_prefill_kernel<64, 4, 1>), grid, dim3(256), 0, s, a, scale_log2);
   if (info) {
     info->name = a.D == 128 ? "attn_prefill_d128" : "attn_prefill_d64";
     info->flops = a.flops;
