@@ -333,28 +333,31 @@ __device__ __forceinline__ float ld_part(__amdgpu_buffer_rsrc_t r, int byte_off)
 
 // Merge the n_splits partials of one query head (row r of ro / rml holds
 // split r) in split order with a running max; 8 splits are loaded together.
+// Splits [0, n_valid) of a row are merged in split order. The loads cover
+// [0, n_load) (n_load >= n_valid, rows that exist in the buffer) and do not
+// depend on n_valid, so they go out without waiting for the context length;
+// rows past n_valid may hold anything and are dropped by selects.
 template <int D>
 __device__ __forceinline__ float merge_splits(__amdgpu_buffer_rsrc_t ro, __amdgpu_buffer_rsrc_t rml,
-                                              int row0, int n_splits, int d) {
+                                              int row0, int n_load, int n_valid, int d) {
   float M = -INFINITY, L = 0.f, O = 0.f;
-  for (int s0 = 0; s0 < n_splits; s0 += 8) {
+  for (int s0 = 0; s0 < n_load; s0 += 8) {
     float ms[8], ls[8], os[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {  // past the last split: re-read it, then ignore
-      const int row = row0 + min(s0 + u, n_splits - 1);
+    for (int u = 0; u < 8; ++u) {  // past n_load: re-read the last row, then ignore
+      const int row = row0 + min(s0 + u, n_load - 1);
       ms[u] = ld_part(rml, row * 8);
       ls[u] = ld_part(rml, row * 8 + 4);
       os[u] = ld_part(ro, (row * D + d) * 4);
     }
-    // branch-free, so that all 24 loads are in flight together; a skipped
-    // split leaves O and L exactly as they were (x 1 + finite x 0)
+    // branch-free, so that all 24 loads are in flight together
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const bool ok = s0 + u < n_splits && ms[u] != -INFINITY;
+      const bool ok = s0 + u < n_valid && ms[u] != -INFINITY;
       const float mn = ok ? fmaxf(M, ms[u]) : M;
       const float wo = ok ? fast_exp2(M - mn) : 1.f, wn = ok ? fast_exp2(ms[u] - mn) : 0.f;
-      O = O * wo + os[u] * wn;
-      L = L * wo + ls[u] * wn;
+      O = ok ? O * wo + os[u] * wn : O;
+      L = ok ? L * wo + ls[u] * wn : L;
       M = mn;
     }
   }
@@ -824,7 +827,8 @@ __global__ __launch_bounds__(D) void attn_decode_combine_kernel(AttnDecodeArgs a
       __builtin_amdgcn_make_buffer_rsrc(a.part_o + base * D, 0, a.max_splits * D * 4, kRawBuffer);
   const __amdgpu_buffer_rsrc_t rml =
       __builtin_amdgcn_make_buffer_rsrc(a.part_ml + base * 2, 0, a.max_splits * 8, kRawBuffer);
-  a.out[(int64_t)b * a.ldo + h * D + d] = f2bf(merge_splits<D>(ro, rml, 0, n_splits, d));
+  a.out[(int64_t)b * a.ldo + h * D + d] =
+      f2bf(merge_splits<D>(ro, rml, 0, a.call_splits, n_splits, d));
 }
 
 namespace {
