@@ -29,8 +29,8 @@ extern "C" {
  * of X zero. This is the projection arithmetic of every decoder layer (QKV,
  * O, gate/up, down) and of the LM head. Shapes with few output tiles split
  * their k range over workgroups; the partial sums go through a workspace
- * that the library allocates once per device (64 MiB + 256 KiB, on the first
- * call) and keeps until the process ends, so calls on one device must not
+ * that the library allocates once per device (128 MiB + 256 KiB, on the
+ * first call) and keeps until the process ends, so calls on one device must not
  * run concurrently. Results are deterministic: the same inputs give the same
  * bits on every call. */
 hs_status hs_k_gemm(const void* X, int64_t ldx, const void* W, void* Y, int64_t ldy,
@@ -96,6 +96,18 @@ hs_status hs_k_attn_decode_rope(const void* qkv, int64_t ldqkv, void* pool,
                                 void* out, int64_t ldo, int32_t B, int32_t n_heads,
                                 int32_t n_kv_heads, int32_t head_dim, int32_t max_blocks,
                                 int32_t max_ctx, void* stream);
+
+/* Greedy sampling of the first token and of every decode step (section 2.1:
+ * the next token is chosen from the logits of the last position): out[r] =
+ * the lowest column index c with logits[r][c] equal to the row's maximum.
+ * logits: device float32 [n_rows][n_cols], row-major, 16-byte aligned;
+ * out: device int32 [n_rows]. Requires n_rows >= 1 and n_cols >= 1 with
+ * n_cols % 4 == 0 (HS_EINVAL otherwise). NaN entries never win; a row of
+ * NaN only gives 0x7FFFFFFF. The call allocates a small device buffer for
+ * the per-chunk candidates, launches the two passes on `stream`, waits for
+ * them and frees the buffer. */
+hs_status hs_k_argmax(const float* logits, int32_t n_rows, int32_t n_cols, int32_t* out,
+                      void* stream);
 
 /* RMSNorm of `rows` rows of width `hidden`: out = x / sqrt(mean(x^2) + eps) * g,
  * bf16 in and out, float32 arithmetic. */

@@ -9,6 +9,7 @@
 #include "../../include/hs_kernel.h"
 #include "hs_host.h"
 #include "hs_kernels.h"
+#include "kernel_entry.h"
 
 using namespace hs;
 
@@ -142,24 +143,59 @@ struct DecodeWs {
 };
 }  // namespace
 
+int64_t hs::attn_decode_ws_floats(int32_t B, int32_t n_heads, int32_t head_dim, int32_t max_ctx) {
+  if (B < 1 || n_heads < 1 || head_dim < 1 || max_ctx < 1) return 0;
+  const int64_t max_splits = (max_ctx + kDecodeSplit - 1) / kDecodeSplit;
+  return (int64_t)B * n_heads * max_splits * (head_dim + 2);
+}
+
+hs_status hs::attn_decode_check(const void* q, const void* pool, const int32_t* block_table,
+                            const int32_t* ctx, const void* out, bool rope, const float* cos_t,
+                            const float* sin_t, int32_t max_pos, int32_t B, int32_t n_heads,
+                            int32_t n_kv_heads, int32_t max_blocks, int32_t max_ctx) {
+  if (!q || !pool || !block_table || !ctx || !out || B < 1 || max_ctx < 1)
+    return fail(HS_EINVAL, "bad arguments");
+  if (n_kv_heads < 1 || n_heads < 1 || n_heads % n_kv_heads)
+    return fail(HS_EINVAL, "bad head counts");
+  if (max_blocks < (max_ctx + 15) / 16) return fail(HS_EINVAL, "block table too narrow");
+  if (rope && (!cos_t || !sin_t || max_pos < max_ctx))
+    return fail(HS_EINVAL, "RoPE tables missing or shorter than max_ctx");
+  return HS_OK;
+}
+
+hs_status hs::attn_decode_run(const void* q, int64_t ldq, const void* pool, bf16_t* pool_w,
+                          const int32_t* block_table, const int32_t* ctx, const float* cos_t,
+                          const float* sin_t, int32_t max_pos, void* out, int64_t ldo, int32_t B,
+                          int32_t n_heads, int32_t n_kv_heads, int32_t head_dim,
+                          int32_t max_blocks, int32_t max_ctx, float* ws, void* stream) {
+  const int max_splits = (max_ctx + kDecodeSplit - 1) / kDecodeSplit;
+  AttnDecodeArgs a{static_cast<const bf16_t*>(q), ldq, static_cast<const bf16_t*>(pool),
+                   block_table, ctx, ws, ws + (int64_t)B * n_heads * max_splits * head_dim,
+                   static_cast<bf16_t*>(out), ldo, B, n_heads, n_kv_heads, head_dim, max_blocks,
+                   max_splits, max_splits, 0.0};
+  a.pool_w = pool_w;
+  a.cos_t = cos_t;
+  a.sin_t = sin_t;
+  a.max_pos = max_pos;
+  return launched(attn_decode(a, static_cast<hipStream_t>(stream), nullptr), "attn_decode");
+}
+
 namespace {
 hs_status attn_decode_entry(const void* q, int64_t ldq, const void* pool, bf16_t* pool_w,
                             const int32_t* block_table, const int32_t* ctx, const float* cos_t,
                             const float* sin_t, int32_t max_pos, void* out, int64_t ldo,
                             int32_t B, int32_t n_heads, int32_t n_kv_heads, int32_t head_dim,
                             int32_t max_blocks, int32_t max_ctx, void* stream) {
-  if (!q || !pool || !block_table || !ctx || !out || B < 1 || max_ctx < 1)
-    return fail(HS_EINVAL, "bad arguments");
-  if (n_kv_heads < 1 || n_heads % n_kv_heads) return fail(HS_EINVAL, "bad head counts");
-  if (max_blocks < (max_ctx + 15) / 16) return fail(HS_EINVAL, "block table too narrow");
-  if (pool_w && (!cos_t || !sin_t || max_pos < max_ctx))
-    return fail(HS_EINVAL, "RoPE tables missing or shorter than max_ctx");
+  const hs_status chk = attn_decode_check(q, pool, block_table, ctx, out, pool_w != nullptr,
+                                          cos_t, sin_t, max_pos, B, n_heads, n_kv_heads,
+                                          max_blocks, max_ctx);
+  if (chk != HS_OK) return chk;
   static DecodeWs ws[64];
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
-    return fail(HS_EHIP, "hipGetDevice failed");
-  const int max_splits = (max_ctx + kDecodeSplit - 1) / kDecodeSplit;
-  const int64_t need = (int64_t)B * n_heads * max_splits * (head_dim + 2);
+  const hipError_t ge = hipGetDevice(&dev);
+  if (ge != hipSuccess || dev < 0 || dev >= 64)
+    return fail(HS_EHIP, std::string("hipGetDevice: ") + hipGetErrorString(ge));
+  const int64_t need = attn_decode_ws_floats(B, n_heads, head_dim, max_ctx);
   DecodeWs& w = ws[dev];
   if (w.floats < need) {
     if (w.buf) {
@@ -172,15 +208,8 @@ hs_status attn_decode_entry(const void* q, int64_t ldq, const void* pool, bf16_t
       return fail(HS_ENOMEM, "attention workspace");
     w.floats = need;
   }
-  AttnDecodeArgs a{static_cast<const bf16_t*>(q), ldq, static_cast<const bf16_t*>(pool),
-                   block_table, ctx, w.buf, w.buf + (int64_t)B * n_heads * max_splits * head_dim,
-                   static_cast<bf16_t*>(out), ldo, B, n_heads, n_kv_heads, head_dim, max_blocks,
-                   max_splits, max_splits, 0.0};
-  a.pool_w = pool_w;
-  a.cos_t = cos_t;
-  a.sin_t = sin_t;
-  a.max_pos = max_pos;
-  return launched(attn_decode(a, static_cast<hipStream_t>(stream), nullptr), "attn_decode");
+  return attn_decode_run(q, ldq, pool, pool_w, block_table, ctx, cos_t, sin_t, max_pos, out, ldo,
+                         B, n_heads, n_kv_heads, head_dim, max_blocks, max_ctx, w.buf, stream);
 }
 }  // namespace
 
@@ -210,6 +239,25 @@ extern "C" hs_status hs_k_attn_decode_rope(const void* qkv, int64_t ldqkv, void*
     return attn_decode_entry(qkv, ldqkv, pool, static_cast<bf16_t*>(pool), block_table, ctx,
                              cos_t, sin_t, max_pos, out, ldo, B, n_heads, n_kv_heads, head_dim,
                              max_blocks, max_ctx, stream);
+  } catch (...) {
+    return fail(HS_EINVAL, "unexpected internal error");
+  }
+}
+
+extern "C" hs_status hs_k_argmax(const float* logits, int32_t n_rows, int32_t n_cols,
+                                 int32_t* out, void* stream) {
+  try {
+    if (!logits || !out || n_rows < 1 || n_cols < 1 || n_cols % 4)
+      return fail(HS_EINVAL, "needs logits, out, n_rows >= 1 and n_cols % 4 == 0");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    int32_t* part = nullptr;
+    const size_t nb = (size_t)n_rows * argmax_chunks(n_cols) * 2 * sizeof(int32_t);
+    if (hipMalloc(reinterpret_cast<void**>(&part), nb) != hipSuccess)
+      return fail(HS_ENOMEM, "device allocation failed");
+    hipError_t e = argmax_rows(logits, n_rows, n_cols, part, out, s, nullptr);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    (void)hipFree(part);
+    return launched(e, "argmax");
   } catch (...) {
     return fail(HS_EINVAL, "unexpected internal error");
   }

@@ -117,6 +117,7 @@ _SIGS = {
     "hs_k_rmsnorm": [_P, _P, _P, C.c_int32, C.c_int32, C.c_float, _P],
     "hs_k_attn_decode": [_P, C.c_int64, _P, _P, _P, _P, C.c_int64, C.c_int32, C.c_int32,
                          C.c_int32, C.c_int32, C.c_int32, C.c_int32, _P],
+    "hs_k_argmax": [_P, C.c_int32, C.c_int32, _P, _P],
     "hs_k_attn_decode_rope": [_P, C.c_int64, _P, _P, _P, _P, _P, C.c_int32, _P, C.c_int64,
                               C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                               _P],
@@ -133,6 +134,14 @@ def lib():
         if not os.path.exists(LIB_PATH):
             raise HSError(HS_EINVAL, f"{LIB_PATH} is missing; build it with "
                           "`python -m paper_2502_15524_amd.build`")
+        # torch ships its own HIP runtime under the same soname as the one
+        # libhs.so links against. Loaded first, torch's copy is the one both
+        # use; loaded the other way round, the process ends up with two
+        # runtimes and the library's sees no device. So torch goes first.
+        try:
+            import torch  # noqa: F401
+        except ImportError:
+            pass
         l = C.CDLL(LIB_PATH)
         for name, args in _SIGS.items():
             f = getattr(l, name)
@@ -372,6 +381,11 @@ def hs_k_attn_decode(q, ldq, pool, block_table, ctx, out, ldo, B, n_heads, n_kv_
     """Decode attention over a paged KV pool; block_table and ctx are device pointers."""
     _check(lib().hs_k_attn_decode(q, ldq, pool, block_table, ctx, out, ldo, B, n_heads,
                                   n_kv_heads, head_dim, max_blocks, max_ctx, stream or None))
+
+
+def hs_k_argmax(logits, n_rows, n_cols, out, stream=0):
+    """Greedy token per row: lowest index of the row's maximum (device pointers)."""
+    _check(lib().hs_k_argmax(logits, n_rows, n_cols, out, stream or None))
 
 
 def hs_k_attn_decode_rope(qkv, ldqkv, pool, block_table, ctx, cos_t, sin_t, max_pos, out, ldo,

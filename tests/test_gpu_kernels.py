@@ -404,3 +404,48 @@ def test_gemm_rejects_unsupported_shapes():
         with pytest.raises(hs.HSError) as e:
             hs.hs_k_gemm(p, ldx, p, p, N, 0, 0, M, N, K, epi)
         assert e.value.code == hs.HS_EINVAL
+
+
+@pytest.mark.parametrize("n_rows,n_cols", [(1, 4), (3, 1024), (2, 4096), (5, 32000),
+                                            (2, 128256), (1, 8196)])
+def test_argmax_ties_lowest_index(n_rows, n_cols):
+    """Greedy sampling: the lowest index of the row maximum, with ties inside a
+    4096-column chunk, across a chunk boundary (the earlier chunk must win)
+    and at the last column; the rows are checked against numpy's argmax,
+    which returns the first maximal index."""
+    torch = G.torch()
+    hs = _hs()
+    rng = np.random.default_rng(n_rows * 31 + n_cols)
+    x = rng.standard_normal((n_rows, n_cols)).astype(np.float32)
+    top = np.float32(50.0)
+    for r in range(n_rows):
+        kind = r % 5
+        if kind == 0:      # tie inside one chunk
+            cols = rng.choice(min(n_cols, 4096), size=min(3, n_cols), replace=False)
+        elif kind == 1:    # tie across the chunk boundary and at the last column
+            cols = [c for c in (4095, 4096, n_cols - 1) if c < n_cols]
+        elif kind == 2:    # maximum only at the last column
+            cols = [n_cols - 1]
+        elif kind == 3:    # every column equal
+            x[r, :] = top
+            cols = []
+        else:              # ties in the last chunk and the first
+            cols = sorted({n_cols - 1, n_cols - 2, 0} & set(range(n_cols)))
+        x[r, list(cols)] = top
+    x[0, -1] = np.inf if n_cols > 8 and n_rows > 2 else x[0, -1]
+    dx = torch.from_numpy(x).cuda()
+    out = torch.full((n_rows,), -1, dtype=torch.int32, device="cuda")
+    hs.hs_k_argmax(dx.data_ptr(), n_rows, n_cols, out.data_ptr(), G.stream_ptr())
+    torch.cuda.synchronize()
+    assert out.cpu().numpy().tolist() == np.argmax(x, axis=1).tolist()
+
+
+def test_argmax_rejects_bad_shapes():
+    torch = G.torch()
+    hs = _hs()
+    x = torch.zeros((2, 8), dtype=torch.float32, device="cuda")
+    out = torch.zeros(2, dtype=torch.int32, device="cuda")
+    for rows, cols in [(0, 8), (2, 0), (2, 6)]:
+        with pytest.raises(hs.HSError) as e:
+            hs.hs_k_argmax(x.data_ptr(), rows, cols, out.data_ptr(), G.stream_ptr())
+        assert e.value.code == hs.HS_EINVAL
