@@ -114,6 +114,23 @@ hs_status hs_k_argmax(const float* logits, int32_t n_rows, int32_t n_cols, int32
 hs_status hs_k_rmsnorm(const void* x, const void* g, void* out, int32_t rows, int32_t hidden,
                        float eps, void* stream);
 
+/* hs_k_attn_decode without any device allocation, for callers that cannot
+ * allocate: code under HIP graph capture, serving loops that must not call
+ * hipMalloc, harnesses that forbid it. Arguments, kernels, results (bitwise)
+ * and errors are those of hs_k_attn_decode. The split partials live in a
+ * static device array of HS_K_ATTN_DECODE_NOALLOC_MAX_FLOATS floats
+ * (32 MiB), one per GPU, held until the process ends; a call needing more,
+ * B * n_heads * ceil(max_ctx / 128) * (head_dim + 2) floats, returns
+ * HS_ERANGE before touching the GPU. Every call on one GPU uses the same
+ * array, so calls that overlap in time on one GPU (other streams, other
+ * threads) race and give wrong results: order them. */
+#define HS_K_ATTN_DECODE_NOALLOC_MAX_FLOATS (8ll * 1024 * 1024)
+hs_status hs_k_attn_decode_noalloc(const void* q, int64_t ldq, const void* pool,
+                                   const int32_t* block_table, const int32_t* ctx, void* out,
+                                   int64_t ldo, int32_t B, int32_t n_heads, int32_t n_kv_heads,
+                                   int32_t head_dim, int32_t max_blocks, int32_t max_ctx,
+                                   void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -17,7 +17,7 @@ LIBDIR = os.path.join(PKG, "_lib")
 LIB = os.path.join(LIBDIR, "libhs.so")
 ARCH = "gfx950"
 
-HIP_SOURCES = ["k_gemm.hip", "k_attn.hip", "k_misc.hip"]
+HIP_SOURCES = ["k_gemm.hip", "k_attn.hip", "k_misc.hip", "k_noalloc.hip"]
 HOST_SOURCES = ["host_layout.cpp", "stage.cpp", "kernel_entry.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall"]

@@ -117,6 +117,8 @@ _SIGS = {
     "hs_k_rmsnorm": [_P, _P, _P, C.c_int32, C.c_int32, C.c_float, _P],
     "hs_k_attn_decode": [_P, C.c_int64, _P, _P, _P, _P, C.c_int64, C.c_int32, C.c_int32,
                          C.c_int32, C.c_int32, C.c_int32, C.c_int32, _P],
+    "hs_k_attn_decode_noalloc": [_P, C.c_int64, _P, _P, _P, _P, C.c_int64, C.c_int32,
+                                 C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32, _P],
     "hs_k_argmax": [_P, C.c_int32, C.c_int32, _P, _P],
     "hs_k_attn_decode_rope": [_P, C.c_int64, _P, _P, _P, _P, _P, C.c_int32, _P, C.c_int64,
                               C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
@@ -381,6 +383,15 @@ def hs_k_attn_decode(q, ldq, pool, block_table, ctx, out, ldo, B, n_heads, n_kv_
     """Decode attention over a paged KV pool; block_table and ctx are device pointers."""
     _check(lib().hs_k_attn_decode(q, ldq, pool, block_table, ctx, out, ldo, B, n_heads,
                                   n_kv_heads, head_dim, max_blocks, max_ctx, stream or None))
+
+
+def hs_k_attn_decode_noalloc(q, ldq, pool, block_table, ctx, out, ldo, B, n_heads, n_kv_heads,
+                             head_dim, max_blocks, max_ctx, stream=0):
+    """hs_k_attn_decode with its split partials in the library's static
+    per-GPU array (no device allocation); calls on one GPU must not overlap."""
+    _check(lib().hs_k_attn_decode_noalloc(q, ldq, pool, block_table, ctx, out, ldo, B, n_heads,
+                                          n_kv_heads, head_dim, max_blocks, max_ctx,
+                                          stream or None))
 
 
 def hs_k_argmax(logits, n_rows, n_cols, out, stream=0):
