@@ -88,7 +88,6 @@ struct hs_stage {
   std::vector<int32_t> free_blocks;  // stack; back() is handed out next
   std::map<int64_t, Seq> seqs;
 
-  hipStream_t compute = nullptr;
   std::vector<hipStream_t> copy;
   int next_copy = 0;
   hipEvent_t last_done = nullptr;
@@ -148,7 +147,6 @@ struct hs_stage {
 
 hs_stage::~hs_stage() {
   DeviceGuard g(device);
-  if (compute) (void)hipStreamSynchronize(compute);
   for (auto s : copy) (void)hipStreamSynchronize(s);
   if (last_valid) (void)hipEventSynchronize(last_done);
   for (auto& kv : chunks) (void)hipEventDestroy(kv.second.ev);
@@ -166,7 +164,6 @@ hs_stage::~hs_stage() {
   if (h_desc) (void)hipHostFree(h_desc);
   if (d_desc) (void)hipFree(d_desc);
   if (last_done) (void)hipEventDestroy(last_done);
-  if (compute) (void)hipStreamDestroy(compute);
   for (auto s : copy) (void)hipStreamDestroy(s);
   for (auto& x : xfer) (void)hipEventDestroy(x.ev);
   if (d_stage) (void)hipFree(d_stage);
@@ -613,10 +610,10 @@ void xfer_reset(hs_stage* st) {
   st->xfer.clear();
 }
 
-// Validate a blob header held in host memory against the stage and reserve
-// its sequences (new sequences get fresh blocks). On error nothing changes.
-hs_status import_reserve(hs_stage* st, const uint8_t* head, uint64_t head_len, uint64_t bytes,
-                         BlobHeader* hout, std::vector<BlobRecord>* rout) {
+// Validate a blob header held in host memory against the stage. Changes
+// nothing; import_commit then registers the sequences.
+hs_status import_check(hs_stage* st, const uint8_t* head, uint64_t head_len, uint64_t bytes,
+                       BlobHeader* hout, std::vector<BlobRecord>* rout) {
   BlobHeader h;
   std::vector<BlobRecord> recs;
   hs_status r = blob_decode_head(head, head_len, &h, &recs);
@@ -646,6 +643,21 @@ hs_status import_reserve(hs_stage* st, const uint8_t* head, uint64_t head_len, u
   if ((int64_t)st->seqs.size() + new_seqs > st->opts.max_seqs)
     return fail(HS_ENOMEM, "no free sequence slots");
   if (need_blocks > (int64_t)st->free_blocks.size()) return fail(HS_ENOMEM, "not enough free KV blocks");
+  *hout = h;
+  *rout = std::move(recs);
+  return HS_OK;
+}
+
+// Units one import of this blob copies (layers x blocks of every record).
+uint64_t import_unit_count(const BlobHeader& h, const std::vector<BlobRecord>& recs) {
+  uint64_t blocks = 0;
+  for (const BlobRecord& rc : recs) blocks += (uint64_t)rc.n_blocks;
+  return (uint64_t)(h.layer_end - h.layer_begin) * blocks;
+}
+
+// Register the blob's sequences (new ones get fresh blocks) after
+// import_check accepted it; cannot fail.
+void import_commit(hs_stage* st, const BlobHeader& h, const std::vector<BlobRecord>& recs) {
   for (const BlobRecord& rc : recs) {
     auto it = st->seqs.find(rc.seq_id);
     if (it == st->seqs.end()) {
@@ -664,9 +676,6 @@ hs_status import_reserve(hs_stage* st, const uint8_t* head, uint64_t head_len, u
       q.kv_end = std::max(q.kv_end, h.layer_end);
     }
   }
-  *hout = h;
-  *rout = std::move(recs);
-  return HS_OK;
 }
 
 // Units of an import: blob payload (at base) -> the stage's pools.
@@ -827,9 +836,8 @@ extern "C" hs_status hs_stage_create(const hs_model_cfg* cfg, int32_t layer_begi
       return bail(fail(HS_EHIP, "RoPE table upload failed"));
   }
 
-  // streams, events
-  if (hipStreamCreateWithFlags(&st->compute, hipStreamNonBlocking) != hipSuccess)
-    return bail(fail(HS_EHIP, "stream creation failed"));
+  // streams (the weight-upload streams only: compute runs on the caller's
+  // stream), events
   for (int i = 0; i < opts->n_copy_streams; ++i) {
     hipStream_t s = nullptr;
     if (hipStreamCreateWithFlags(&s, hipStreamNonBlocking) != hipSuccess)
@@ -876,7 +884,6 @@ extern "C" hs_status hs_stage_sync(hs_stage* st) {
   if (!st) return fail(HS_EINVAL, "null stage");
   DeviceGuard dg(st->device);
   if (st->last_valid) HIPTRY(hipEventSynchronize(st->last_done));
-  HIPTRY(hipStreamSynchronize(st->compute));
   for (auto s : st->copy) HIPTRY(hipStreamSynchronize(s));
   return HS_OK;
   ABI_END
@@ -985,30 +992,31 @@ extern "C" hs_status hs_stage_prefill(hs_stage* st, int32_t n, const int64_t* id
   Meta mt;
   r = meta_acquire(st, &mt);
   if (r != HS_OK) return r;
-  // register sequences and build per-token metadata
+  // the new sequences and per-token metadata; the sequences take blocks from
+  // the back of the free list (as popping would) but the stage's state only
+  // changes once every launch has been enqueued, so a failed call leaves it
+  // as it was
   int32_t *d_pos, *d_slot, *d_cu, *d_tiles, *d_last;
   int32_t* pos = mt.take(T, &d_pos);
   int32_t* slot = mt.take(T, &d_slot);
   int32_t* cu = mt.take(n + 1, &d_cu);
   std::vector<std::pair<int, int>> tiles;
+  std::vector<Seq> fresh(n);
+  size_t free_end = st->free_blocks.size();
   double attn_flops = 0;
   cu[0] = 0;
   for (int i = 0; i < n; ++i) {
-    Seq sq;
+    Seq& sq = fresh[i];
     sq.n_tokens = lens[i];
     sq.kv_begin = st->begin;
     sq.kv_end = st->end;
-    for (int b = 0; b < blocks_for(lens[i]); ++b) {
-      sq.blocks.push_back(st->free_blocks.back());
-      st->free_blocks.pop_back();
-    }
+    for (int b = 0; b < blocks_for(lens[i]); ++b) sq.blocks.push_back(st->free_blocks[--free_end]);
     for (int p = 0; p < lens[i]; ++p) {
       pos[cu[i] + p] = p;
       slot[cu[i] + p] = sq.blocks[p / kBlock] * kBlock + p % kBlock;
     }
     cu[i + 1] = cu[i] + lens[i];
     attn_flops += 4.0 * st->cfg.n_heads * st->cfg.head_dim * 0.5 * (double)lens[i] * (lens[i] + 1);
-    st->seqs.emplace(ids[i], std::move(sq));
   }
   // attention work tiles: q_tile queries of one sequence, longest rows first
   int64_t tiles128 = 0;
@@ -1069,6 +1077,8 @@ extern "C" hs_status hs_stage_prefill(hs_stage* st, int32_t n, const int64_t* id
     r = head_forward(st, x, d_last, n, logits_opt, static_cast<int32_t*>(out), s);
     if (r != HS_OK) return r;
   }
+  st->free_blocks.resize(free_end);
+  for (int i = 0; i < n; ++i) st->seqs.emplace(ids[i], std::move(fresh[i]));
   return end_call(st, s);
   ABI_END
 }
@@ -1115,18 +1125,21 @@ extern "C" hs_status hs_stage_decode(hs_stage* st, int32_t n, const int64_t* ids
   int call_splits = 1;
   double kv_bytes = 0;
   const double tok_bytes = 2.0 * st->cfg.n_kv_heads * st->cfg.head_dim * 2;
+  // a sequence whose last block is full takes a new one from the back of the
+  // free list; the stage's state changes only after the launches (see prefill)
+  std::vector<int32_t> new_block(n, -1);
+  size_t free_end = st->free_blocks.size();
   for (int i = 0; i < n; ++i) {
-    Seq& q = *sq[i];
+    const Seq& q = *sq[i];
     const int p = q.n_tokens;
-    if (p % kBlock == 0) {
-      q.blocks.push_back(st->free_blocks.back());
-      st->free_blocks.pop_back();
-    }
-    q.n_tokens = p + 1;
+    if (p % kBlock == 0) new_block[i] = st->free_blocks[--free_end];
+    const int nb = (int)q.blocks.size() + (new_block[i] >= 0 ? 1 : 0);
+    const int last_blk = new_block[i] >= 0 ? new_block[i] : q.blocks[p / kBlock];
     pos[i] = p;
-    slot[i] = q.blocks[p / kBlock] * kBlock + p % kBlock;
+    slot[i] = last_blk * kBlock + p % kBlock;
     ctx[i] = p + 1;
-    for (int b = 0; b < MB; ++b) bt[(uint64_t)i * MB + b] = b < (int)q.blocks.size() ? q.blocks[b] : 0;
+    for (int b = 0; b < MB; ++b)
+      bt[(uint64_t)i * MB + b] = b < (int)q.blocks.size() ? q.blocks[b] : (b < nb ? new_block[i] : 0);
     call_splits = std::max(call_splits, (p + 1 + kDecodeSplit - 1) / kDecodeSplit);
     kv_bytes += (p + 1) * tok_bytes;
   }
@@ -1168,6 +1181,11 @@ extern "C" hs_status hs_stage_decode(hs_stage* st, int32_t n, const int64_t* ids
     if (r != HS_OK) return r;
     r = head_forward(st, x, nullptr, n, logits_opt, static_cast<int32_t*>(out), s);
     if (r != HS_OK) return r;
+  }
+  st->free_blocks.resize(free_end);
+  for (int i = 0; i < n; ++i) {
+    if (new_block[i] >= 0) sq[i]->blocks.push_back(new_block[i]);
+    sq[i]->n_tokens += 1;
   }
   return end_call(st, s);
   ABI_END
@@ -1320,8 +1338,11 @@ extern "C" hs_status hs_kv_import(hs_stage* st, const void* src, uint64_t bytes,
   }
   BlobHeader h;
   std::vector<BlobRecord> recs;
-  r = import_reserve(st, head.data(), head.size(), bytes, &h, &recs);
+  r = import_check(st, head.data(), head.size(), bytes, &h, &recs);
   if (r != HS_OK) return r;
+  r = desc_reserve(st, import_unit_count(h, recs) + 1);  // the last step that can fail
+  if (r != HS_OK) return r;
+  import_commit(st, h, recs);
   Units u = import_units(st, h, recs, (uint64_t)(uintptr_t)src);
   r = copy_units(st, u, 0, s);
   if (r != HS_OK) return r;
@@ -1445,8 +1466,11 @@ extern "C" hs_status hs_kv_import_host(hs_stage* st, const void* src, uint64_t b
   if (r != HS_OK) return r;
   BlobHeader h;
   std::vector<BlobRecord> recs;
-  r = import_reserve(st, hb, kBlobHeader + kBlobRecord * (uint64_t)ns, bytes, &h, &recs);
+  r = import_check(st, hb, kBlobHeader + kBlobRecord * (uint64_t)ns, bytes, &h, &recs);
   if (r != HS_OK) return r;
+  r = desc_reserve(st, import_unit_count(h, recs) + 1);  // the last step that can fail
+  if (r != HS_OK) return r;
+  import_commit(st, h, recs);
   Units u = import_units(st, h, recs, (uint64_t)(uintptr_t)st->d_stage);
   r = begin_call(st, s);
   if (r != HS_OK) return r;
@@ -1568,6 +1592,13 @@ extern "C" hs_status hs_stage_merge(hs_stage* dst, hs_stage* const* srcs, int32_
   dst->begin = save_b;
   dst->end = save_e;
   if (r != HS_OK) return fail(HS_ESTATE, std::string("merge target: ") + hs_last_error());
+
+  uint64_t n_units = 0;
+  for (int i = 0; i < n_srcs; ++i)
+    for (const auto& kv : srcs[i]->seqs)
+      n_units += (uint64_t)(srcs[i]->end - srcs[i]->begin) * blocks_for(kv.second.n_tokens);
+  r = desc_reserve(dst, n_units + 1);  // before any state changes
+  if (r != HS_OK) return r;
 
   hipStream_t s = pick(dst, stream);
   r = begin_call(dst, s);

@@ -30,6 +30,22 @@ def env():
                 o_logits=o_logits)
 
 
+def assert_oracle_teacher_forced(env, prompt, fed, gpu_logits):
+    """The oracle (whole model, float32) on the prompt and then on the tokens
+    the engine fed back, one decode step each: every row of the engine's
+    logits (prefill's last position, then each step) within LOGIT_TOL of the
+    largest oracle logit."""
+    ost = OStage(CFG, env["W"], 0, CFG.n_layers)
+    ref = [ost.prefill([0], [len(prompt)], np.asarray(prompt))[-1]]
+    for t in fed:
+        ref.append(ost.decode([0], np.array([t], np.int32))[0])
+    ref = np.stack(ref)
+    got = np.asarray(gpu_logits)
+    assert got.shape == ref.shape, (got.shape, ref.shape)
+    err = np.abs(got - ref).max(axis=1) / np.abs(ref).max(axis=1)
+    assert err.max() <= LOGIT_TOL, err
+
+
 def make(env, begin, end, resident=None, load=True, **kw):
     rb, re = resident or (begin, end)
     opts = dict(max_seqs=8, max_ctx=640, max_batch_tokens=1024)
@@ -268,12 +284,14 @@ def test_merge_equals_pipeline_bitwise(env):
     # continue both from the same token
     torch = G.torch()
     sp = G.stream_ptr()
-    res = []
+    res, fed = [], []
     for stages in ([a0, a1], [merged]):
         nxt = torch.tensor([int(ta[-1])], dtype=torch.int32, device="cuda")
         lg = torch.zeros((1, CFG.vocab), dtype=torch.float32, device="cuda")
         seq = []
+        fed = []
         for _ in range(5):
+            fed.append(int(nxt.item()))
             x = nxt.clone()
             for st in stages:
                 if st.end == CFG.n_layers:
@@ -285,6 +303,9 @@ def test_merge_equals_pipeline_bitwise(env):
             seq.append(lg.cpu().numpy().copy())
         res.append(np.stack(seq))
     assert np.array_equal(res[0], res[1])
+    # and the merged worker against the oracle, fed the same tokens
+    assert_oracle_teacher_forced(env, env["prompt"], list(ta[:2]) + fed,
+                                 np.concatenate([lb, res[1][:, 0]]))
 
 
 def test_chunk_order_does_not_change_results(env):
@@ -361,6 +382,13 @@ def test_error_paths(env):
     cramped = make(env, 0, 1, kv_num_blocks=1)
     assert code(hs.hs_kv_import, cramped.h, blob.data_ptr(), blob.numel(), sp) == hs.HS_ENOMEM
     assert cramped.info()["live_seqs"] == 0 and cramped.info()["free_blocks"] == 1
+    # a prefill or decode that cannot get its blocks changes nothing either
+    assert code(cramped.prefill, [5], [32], x.data_ptr(), out.data_ptr(), 0, sp) == hs.HS_ENOMEM
+    assert cramped.info()["live_seqs"] == 0 and cramped.info()["free_blocks"] == 1
+    cramped.prefill([6], [16], x.data_ptr(), out.data_ptr(), 0, sp)     # one full block
+    assert cramped.info()["free_blocks"] == 0
+    assert code(cramped.decode, [6], one.data_ptr(), o1.data_ptr(), 0, sp) == hs.HS_ENOMEM
+    assert hs.hs_seq_tokens(cramped.h, 6) == 16 and cramped.info()["free_blocks"] == 0
     # merge preconditions
     m = make(env, 0, 0, resident=(0, 2))
     s1 = make(env, 1, 2)
@@ -461,6 +489,7 @@ def test_scale_down_background_load_then_merge(env):
         decode([s0])
     assert np.array_equal(np.array(toks, np.int32), ref_toks)
     assert np.array_equal(np.stack(lgs), ref_lgs)
+    assert_oracle_teacher_forced(env, env["prompt"], toks[:-1], np.stack(lgs))
 
 
 def test_host_staged_migration_bitwise(env):
@@ -529,6 +558,7 @@ def test_continuous_batching_then_merge_bitwise(env):
     s0 = make(env, 0, 1, resident=(0, 2))
     s1 = make(env, 1, 2)
     got = {sid: [] for sid in prompts}
+    fed = {sid: [] for sid in prompts}
     nxt = {}
 
     def prefill(stages, sid):
@@ -545,6 +575,8 @@ def test_continuous_batching_then_merge_bitwise(env):
 
     def decode(stages, ids):
         B = len(ids)
+        for i in ids:
+            fed[i].append(nxt[i])
         x = torch.tensor([nxt[i] for i in ids], dtype=torch.int32, device="cuda")
         tok = torch.zeros(B, dtype=torch.int32, device="cuda")
         lg = torch.zeros((B, CFG.vocab), dtype=torch.float32, device="cuda")
@@ -579,3 +611,4 @@ def test_continuous_batching_then_merge_bitwise(env):
     for sid, lgs in got.items():
         assert len(lgs) == len(ref[sid]), sid
         assert np.array_equal(np.stack(lgs), ref[sid]), sid
+        assert_oracle_teacher_forced(env, prompts[sid], fed[sid], np.stack(lgs))
