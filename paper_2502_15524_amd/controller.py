@@ -1,7 +1,7 @@
-"""Cold-start controller arithmetic: TTFT / TPOT prediction, resource
-allocation and network-contention-aware placement (section 4 and 5 of the
-paper), calibrated with this engine's measured prefill, decode and host-link
-figures. Pure host code; nothing here touches the GPU.
+"""Cold-start controller arithmetic: TTFT / TPOT prediction (section 4.1,
+Eq. 1 and 2; Eq. 5 of section 5.2), resource allocation (section 4.1) and
+network-contention-aware placement (section 4.2, Eq. 3 and 4), calibrated
+with this engine's measured prefill, decode and host-link figures. Pure host code; nothing here touches the GPU.
 
 Notation follows the paper: t_c container creation + runtime initialisation,
 t_n network transfer between pipeline workers, t_p prefill and t_d decode
@@ -18,8 +18,8 @@ from typing import Dict, List, Sequence, Tuple
 
 @dataclasses.dataclass(frozen=True)
 class History:
-    """Historical time costs of a model (section 4.2). t_cc, t_cu, t_l split
-    t_c for the overlapped prediction of section 5.3 (container creation,
+    """Historical time costs of a model (section 4.1). t_cc, t_cu, t_l split
+    t_c for the overlapped prediction of section 5.2 (container creation,
     GPU context initialisation, library loading)."""
     t_c: float
     t_n: float
@@ -101,53 +101,70 @@ class Choice:
         return sum(1 for x in self.servers if x.workers > 0)
 
 
-def _order(x: Server):
-    """Server preference: fastest fetch-and-load first; among equals, a free
-    GPU before a busy one."""
-    return (x.ratio, x.workers)
+def _placement(servers: Sequence[Server], M: float, s: int, w: int):
+    """The server group for s workers of which w hold the whole model.
+
+    TTFT (Eq. 1) depends on the group only through its slowest fetch-and-load
+    rate, so the group is a bottleneck choice: the smallest rate limit r such
+    that, among the servers with ratio <= r, at least w can hold the model
+    (M) and at least s can hold a 1/s part of it (every server that holds M
+    holds M/s too). Under that limit, the fewest busy GPUs: the w
+    whole-model slots take free GPUs first, then the remaining s - w slots
+    do; within each, the faster server first. Returns None if no group
+    exists."""
+    part = M / s
+    fits_full = [x for x in servers if x.free_mem >= M]
+    fits_part = [x for x in servers if x.free_mem >= part]
+    if len(fits_full) < w or len(fits_part) < s:
+        return None
+    for r in sorted({x.ratio for x in fits_part}):
+        full = [x for x in fits_full if x.ratio <= r]
+        usable = [x for x in fits_part if x.ratio <= r]
+        if len(full) >= w and len(usable) >= s:
+            break
+    else:
+        return None
+    prefer = lambda x: (x.workers > 0, x.ratio)   # noqa: E731  free GPU, then faster
+    chosen = sorted(full, key=prefer)[:w]
+    rest = sorted((x for x in usable if x not in chosen), key=prefer)[:s - w]
+    return tuple(chosen) + tuple(rest)
 
 
 def enumerate_choices(h: History, M: float, servers: Sequence[Server],
                       max_s: int = 4) -> List[Choice]:
-    """Every deployment choice Algorithm 1 considers, with its predictions:
-    for each s and w, the w full-memory servers with the smallest 1/b + 1/p,
-    then the s - w best of the remaining servers that fit M/s (ties go to
-    GPUs with fewer running workers)."""
+    """Every deployment choice with its TTFT and TPOT predictions (Eq. 1 and
+    2): pipeline sizes s = 1 .. max_s (the paper caps it at 4), w = 0 .. s
+    whole-model workers, each with the group `_placement` picks; choices
+    without a feasible group are left out."""
     out = []
     for s in range(1, max_s + 1):
-        for w in range(0, s + 1):
-            full = sorted((x for x in servers if x.free_mem >= M), key=_order)
-            if len(full) < w:
-                continue
-            low_only = [x for x in servers if M / s <= x.free_mem < M]
-            rest = sorted(low_only + full[w:], key=_order)
-            if len(rest) < s - w:
-                continue
-            g = tuple(full[:w]) + tuple(rest[:s - w])
-            out.append(Choice(s, w, g, predict_ttft(h, M, s, w, g), predict_tpot(h, s, w)))
+        for w in range(s + 1):
+            g = _placement(servers, M, s, w)
+            if g is not None:
+                out.append(Choice(s, w, g, predict_ttft(h, M, s, w, g), predict_tpot(h, s, w)))
     return out
 
 
 def allocate(h: History, M: float, servers: Sequence[Server], slo_ttft: float,
              slo_tpot: float, max_s: int = 4) -> Choice:
-    """Algorithm 1. Among the choices meeting both SLOs, take the one that
-    places the fewest workers on already-busy GPUs, then the one reserving
-    the least GPU memory, then the smallest s. Without any feasible choice,
-    a single full-memory worker on the best server."""
-    feasible = [c for c in enumerate_choices(h, M, servers, max_s)
-                if c.ttft <= slo_ttft and c.tpot <= slo_tpot]
-    if not feasible:
-        full = sorted((x for x in servers if x.free_mem >= M), key=_order)
-        if not full:
-            raise ValueError("no server fits the whole model")
-        g = (full[0],)
-        return Choice(1, 1, g, predict_ttft(h, M, 1, 1, g), predict_tpot(h, 1, 1))
-    return min(feasible, key=lambda c: (c.sharing, c.memory, c.s))
+    """Resource allocation (section 4.1): among the choices whose predicted
+    TTFT and TPOT meet the SLOs, the one with the fewest workers on busy GPUs
+    (the paper prefers free GPUs), then the least GPU memory reserved, then
+    the smallest pipeline. If none meets them, one worker holding the whole
+    model on the server that fetches and loads it fastest."""
+    ok = [c for c in enumerate_choices(h, M, servers, max_s)
+          if c.ttft <= slo_ttft and c.tpot <= slo_tpot]
+    if ok:
+        return min(ok, key=lambda c: (c.sharing, c.memory, c.s))
+    g = _placement(servers, M, 1, 1)
+    if g is None:
+        raise ValueError("no server fits the whole model")
+    return Choice(1, 1, g, predict_ttft(h, M, 1, 1, g), predict_tpot(h, 1, 1))
 
 
 class ServerBandwidth:
     """Network-contention-aware placement bookkeeping of one server (section
-    4.3): its cold-start workers share bandwidth B equally; each has a
+    4.2): its cold-start workers share bandwidth B equally; each has a
     fetching deadline D_i and a pending model size S_i."""
 
     def __init__(self, B: float):

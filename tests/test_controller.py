@@ -84,6 +84,31 @@ def test_server_selection_is_the_best_possible_for_every_s_and_w():
     assert seen == possible
 
 
+def test_placement_takes_fewest_busy_gpus_at_the_best_bottleneck():
+    """Brute force over random clusters: each (s, w) group reaches the
+    smallest possible slowest fetch-and-load rate, and among the groups that
+    reach it, places the fewest workers on busy GPUs."""
+    import random
+    rnd = random.Random(7)
+    for trial in range(60):
+        cluster = [srv(chr(97 + i), b=rnd.choice([1e9, 2e9, 4e9]), p=rnd.choice([10e9, 25e9]),
+                       mem=rnd.choice([4e9, 8e9, 16e9, 80e9]), workers=rnd.choice([0, 0, 1, 2]))
+                   for i in range(6)]
+        for c in enumerate_choices(H, M, cluster):
+            best_r, best_busy = None, None
+            for group in itertools.permutations(cluster, c.s):
+                if not (all(x.free_mem >= M for x in group[:c.w]) and
+                        all(x.free_mem >= M / c.s for x in group[c.w:])):
+                    continue
+                r = max(x.ratio for x in group)
+                busy = sum(x.workers > 0 for x in group)
+                if best_r is None or r < best_r or (r == best_r and busy < best_busy):
+                    best_r, best_busy = r, busy
+            assert max(x.ratio for x in c.servers) == best_r, (trial, c.s, c.w)
+            assert c.sharing == best_busy, (trial, c.s, c.w)
+            assert len(set(x.name for x in c.servers)) == c.s
+
+
 def test_allocation_meets_slos_with_least_memory_on_free_gpus():
     cluster = [srv(c) for c in "abcd"]
     c = allocate(H, M, cluster, slo_ttft=6.0, slo_tpot=0.2)
