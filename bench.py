@@ -457,16 +457,20 @@ def bench_c2(args):
     stream.synchronize()
     exp_ms = ev0.elapsed_time(ev1) / reps
     dst = pipeline.Stage(cfg, b, e, max_seqs=4, max_ctx=max_ctx, max_batch_tokens=P)
-    imp = []
-    for _ in range(reps):
+    head = hs.hs_kv_export_head(st.h, [i])
+    imp, imp1 = [], []
+    for r in range(2 * reps):
         ev0.record(stream)
-        hs.hs_kv_import(dst.h, blob.data_ptr(), size, sp)
+        if r % 2:       # header read back from the device blob
+            hs.hs_kv_import(dst.h, blob.data_ptr(), size, sp)
+        else:           # header handed over by the exporter
+            hs.hs_kv_import_many(dst.h, [(blob.data_ptr(), size, head)], sp)
         ev1.record(stream)
         stream.synchronize()
-        imp.append(ev0.elapsed_time(ev1))
+        (imp1 if r % 2 else imp).append(ev0.elapsed_time(ev1))
         hs.hs_seq_free(dst.h, i)
     imp_ms = statistics.median(imp)
-    used = size - 256
+    used = size - len(head)
     log(f"[bench] KV export {2 * used / (exp_ms / 1e3) / 1e9:.0f} GB/s, "
         f"import {2 * used / (imp_ms / 1e3) / 1e9:.0f} GB/s ({used / 1e6:.1f} MB)")
     dst.close()
@@ -514,6 +518,7 @@ def bench_c2(args):
         "decode_roofline": hbm_roofline(dstats, "decode"),
         "kv_export_GBps": round(2 * used / (exp_ms / 1e3) / 1e9, 1),
         "kv_import_GBps": round(2 * used / (imp_ms / 1e3) / 1e9, 1),
+        "kv_import_with_readback_GBps": round(2 * used / (statistics.median(imp1) / 1e3) / 1e9, 1),
     }
     st.close()
     img.close()
@@ -723,7 +728,7 @@ def bench_pipeline(wl, args, n_dec=None, oracle_sample=False):
     if merge:
         # KV export of every stage to device blobs, and import of all of them
         # into a fresh worker holding every layer's pools
-        blobs, exp_ms, moved = [], [], 0
+        blobs, heads, exp_ms, moved = [], [], [], 0
         for st in stages:
             size = hs.hs_kv_export_size(st.h, ids)
             blob = torch.empty(size, dtype=torch.uint8, device=dev)
@@ -731,17 +736,23 @@ def bench_pipeline(wl, args, n_dec=None, oracle_sample=False):
             ms, _ = timed(lambda: hs.hs_kv_export(st.h, ids, blob.data_ptr(), size, sp), 5)
             exp_ms.append(ms)
             blobs.append((blob, size))
-            moved += size - 256
+            heads.append(hs.hs_kv_export_head(st.h, ids))
+            moved += size - len(heads[-1])
         tgt = pipeline.Stage(cfg, 0, cfg.n_layers, max_seqs=B + 2, max_ctx=max_ctx,
                              max_batch_tokens=T)
-        imp_ms = []
-        for r in range(3):
+        many = [(b.data_ptr(), n, hd) for (b, n), hd in zip(blobs, heads)]
+        imp_ms, imp1_ms = [], []
+        for r in range(4):
             if r:
                 for i in ids:
                     hs.hs_seq_free(tgt.h, i)
-            ms_r, _ = timed(lambda: [hs.hs_kv_import(tgt.h, b.data_ptr(), n, sp)
-                                     for b, n in blobs], 1)
-            imp_ms.append(ms_r)
+            if r % 2:        # one hs_kv_import per blob (each reads its header back)
+                ms_r, _ = timed(lambda: [hs.hs_kv_import(tgt.h, b.data_ptr(), n, sp)
+                                         for b, n in blobs], 1)
+                imp1_ms.append(ms_r)
+            else:            # all blobs in one call, headers from the exporters
+                ms_r, _ = timed(lambda: hs.hs_kv_import_many(tgt.h, many, sp), 1)
+                imp_ms.append(ms_r)
         # host-staged form: each stage's blob leaves the GPU in 64 MiB chunks
         # into pinned host memory, and the target loads them back chunk by
         # chunk (the cross-machine path; bounded by the host link)
@@ -779,9 +790,11 @@ def bench_pipeline(wl, args, n_dec=None, oracle_sample=False):
                 copy_ms += ms_c
                 del dst_b
         del blobs
+        ms_imp1 = statistics.median(imp1_ms)
         log(f"[bench] KV export {moved / 1e9:.2f} GB in {ms_exp:.2f} ms "
             f"({2 * moved / (ms_exp / 1e3) / 1e9:,.0f} GB/s), import {ms_imp:.2f} ms "
-            f"({2 * moved / (ms_imp / 1e3) / 1e9:,.0f} GB/s); a plain device copy of the "
+            f"({2 * moved / (ms_imp / 1e3) / 1e9:,.0f} GB/s; blob by blob with header "
+            f"read-backs {ms_imp1:.2f} ms); a plain device copy of the "
             f"same blobs {copy_ms:.2f} ms ({2 * moved / (copy_ms / 1e3) / 1e9:,.0f} GB/s)")
         # the merge itself: stage 0 takes over every layer (drain, block
         # copies into its pools, serving range extended), then decodes alone
@@ -804,6 +817,7 @@ def bench_pipeline(wl, args, n_dec=None, oracle_sample=False):
                     "bytes_per_op": 2 * moved,
                     "device_copy_ceiling_GBps": round(2 * moved / (copy_ms / 1e3) / 1e9, 1)}
         res_extra = {"kv_export_ms": round(ms_exp, 3), "kv_import_ms": round(ms_imp, 3),
+                     "kv_import_blob_by_blob_ms": round(ms_imp1, 3),
                      "device_copy_same_bytes_ms": round(copy_ms, 3),
                      "kv_bytes": moved,
                      "kv_export_GBps": round(2 * moved / (ms_exp / 1e3) / 1e9, 1),

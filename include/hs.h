@@ -308,6 +308,33 @@ hs_status hs_kv_export(hs_stage* st, int32_t n_seqs, const int64_t* seq_ids,
 hs_status hs_kv_import(hs_stage* st, const void* src, uint64_t bytes,
                        void* stream);
 
+/* The first bytes of the blob hs_kv_export would write for these sequences
+ * now (its 64-byte header, the per-sequence records and the zero padding up
+ * to the payload), written to host memory `host_dst` (`cap` bytes; any host
+ * memory). *written receives their length (payload_offset); HS_ERANGE if cap
+ * is smaller. It lets a worker that exports hand the importer a host copy of
+ * the blob's description with the device blob (section 6.2: the migration
+ * thread sends the blocks' descriptions along with the blocks), so that the
+ * import reads nothing back from the device. No GPU work.
+ * Errors: HS_EINVAL (ids), HS_ERANGE. */
+hs_status hs_kv_export_head(const hs_stage* st, int32_t n_seqs, const int64_t* seq_ids,
+                            void* host_dst, uint64_t cap, uint64_t* written);
+
+/* Import n_blobs device blobs in one call: one upload of copy descriptors
+ * and one copy launch for all of them, no device-to-host read and no host
+ * wait. srcs[i] (device memory, 16-byte aligned, bytes[i] long) is a blob
+ * as hs_kv_export writes it; heads[i] (host memory, head_bytes[i] bytes) must
+ * hold that blob's first bytes, at least its header and records, as
+ * hs_kv_export_head returns them (the call trusts them to describe srcs[i]).
+ * The blobs are applied in order: blob i is validated as hs_kv_import would
+ * validate it after blobs 0 .. i-1, so blobs of adjacent layer ranges of the
+ * same sequences (one per source stage) build up each sequence's cache.
+ * Every blob is validated before anything is enqueued; on error nothing
+ * changes. Errors: those of hs_kv_import (the message names the blob). */
+hs_status hs_kv_import_many(hs_stage* st, int32_t n_blobs, const void* const* srcs,
+                            const uint64_t* bytes, const void* const* heads,
+                            const uint64_t* head_bytes, void* stream);
+
 /* Host-staged (streaming) migration, the form that crosses machines
  * (section 6.2: blocks leave the GPU in chunks that are sent on as soon as
  * they reach host memory, and on the receiving worker each arriving chunk

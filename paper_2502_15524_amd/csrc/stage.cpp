@@ -610,9 +610,15 @@ void xfer_reset(hs_stage* st) {
   st->xfer.clear();
 }
 
-// Validate a blob header held in host memory against the stage. Changes
-// nothing; import_commit then registers the sequences.
-hs_status import_check(hs_stage* st, const uint8_t* head, uint64_t head_len, uint64_t bytes,
+// The sequence table and free-block list an import works on: the stage's
+// own, or copies when several blobs are validated before any of them counts.
+typedef std::map<int64_t, Seq> SeqTable;
+
+// Validate a blob header held in host memory against the stage's geometry
+// and the given sequence table. Changes nothing; import_commit then
+// registers the sequences.
+hs_status import_check(const hs_stage* st, const SeqTable& seqs, size_t n_free,
+                       const uint8_t* head, uint64_t head_len, uint64_t bytes,
                        BlobHeader* hout, std::vector<BlobRecord>* rout) {
   BlobHeader h;
   std::vector<BlobRecord> recs;
@@ -627,8 +633,8 @@ hs_status import_check(hs_stage* st, const uint8_t* head, uint64_t head_len, uin
   int64_t need_blocks = 0, new_seqs = 0;
   for (const BlobRecord& rc : recs) {
     if (rc.n_tokens > st->opts.max_ctx) return fail(HS_EINVAL, "blob sequence longer than max_ctx");
-    auto it = st->seqs.find(rc.seq_id);
-    if (it == st->seqs.end()) {
+    auto it = seqs.find(rc.seq_id);
+    if (it == seqs.end()) {
       need_blocks += rc.n_blocks;
       ++new_seqs;
     } else {
@@ -640,9 +646,9 @@ hs_status import_check(hs_stage* st, const uint8_t* head, uint64_t head_len, uin
         return fail(HS_EINVAL, "blob layers are not adjacent to the sequence's cached layers");
     }
   }
-  if ((int64_t)st->seqs.size() + new_seqs > st->opts.max_seqs)
+  if ((int64_t)seqs.size() + new_seqs > st->opts.max_seqs)
     return fail(HS_ENOMEM, "no free sequence slots");
-  if (need_blocks > (int64_t)st->free_blocks.size()) return fail(HS_ENOMEM, "not enough free KV blocks");
+  if (need_blocks > (int64_t)n_free) return fail(HS_ENOMEM, "not enough free KV blocks");
   *hout = h;
   *rout = std::move(recs);
   return HS_OK;
@@ -657,19 +663,20 @@ uint64_t import_unit_count(const BlobHeader& h, const std::vector<BlobRecord>& r
 
 // Register the blob's sequences (new ones get fresh blocks) after
 // import_check accepted it; cannot fail.
-void import_commit(hs_stage* st, const BlobHeader& h, const std::vector<BlobRecord>& recs) {
+void import_commit(SeqTable& seqs, std::vector<int32_t>& free_blocks, const BlobHeader& h,
+                   const std::vector<BlobRecord>& recs) {
   for (const BlobRecord& rc : recs) {
-    auto it = st->seqs.find(rc.seq_id);
-    if (it == st->seqs.end()) {
+    auto it = seqs.find(rc.seq_id);
+    if (it == seqs.end()) {
       Seq q;
       q.n_tokens = rc.n_tokens;
       q.kv_begin = h.layer_begin;
       q.kv_end = h.layer_end;
       for (int b = 0; b < rc.n_blocks; ++b) {
-        q.blocks.push_back(st->free_blocks.back());
-        st->free_blocks.pop_back();
+        q.blocks.push_back(free_blocks.back());
+        free_blocks.pop_back();
       }
-      st->seqs.emplace(rc.seq_id, std::move(q));
+      seqs.emplace(rc.seq_id, std::move(q));
     } else {
       Seq& q = it->second;
       q.kv_begin = std::min(q.kv_begin, h.layer_begin);
@@ -679,20 +686,19 @@ void import_commit(hs_stage* st, const BlobHeader& h, const std::vector<BlobReco
 }
 
 // Units of an import: blob payload (at base) -> the stage's pools.
-Units import_units(hs_stage* st, const BlobHeader& h, const std::vector<BlobRecord>& recs,
-                   uint64_t base) {
-  Units u;
+void import_units(const hs_stage* st, const SeqTable& seqs, const BlobHeader& h,
+                  const std::vector<BlobRecord>& recs, uint64_t base, Units* out) {
+  Units& u = *out;
   uint64_t unit = 0;
   for (int l = h.layer_begin; l < h.layer_end; ++l)
     for (const BlobRecord& rc : recs) {
-      const Seq& q = st->seqs.at(rc.seq_id);
+      const Seq& q = seqs.at(rc.seq_id);
       for (int b = 0; b < rc.n_blocks; ++b, ++unit) {
         u.src.push_back(base + h.payload_offset + unit * st->unit_bytes);
         u.dst.push_back((uint64_t)(uintptr_t)pool(st, l) + (uint64_t)q.blocks[b] * st->unit_bytes);
         u.valid.push_back(kBlock);
       }
     }
-  return u;
 }
 
 bool same_model(const hs_model_cfg& a, const hs_model_cfg& b) {
@@ -1338,12 +1344,75 @@ extern "C" hs_status hs_kv_import(hs_stage* st, const void* src, uint64_t bytes,
   }
   BlobHeader h;
   std::vector<BlobRecord> recs;
-  r = import_check(st, head.data(), head.size(), bytes, &h, &recs);
+  r = import_check(st, st->seqs, st->free_blocks.size(), head.data(), head.size(), bytes, &h,
+                   &recs);
   if (r != HS_OK) return r;
   r = desc_reserve(st, import_unit_count(h, recs) + 1);  // the last step that can fail
   if (r != HS_OK) return r;
-  import_commit(st, h, recs);
-  Units u = import_units(st, h, recs, (uint64_t)(uintptr_t)src);
+  import_commit(st->seqs, st->free_blocks, h, recs);
+  Units u;
+  import_units(st, st->seqs, h, recs, (uint64_t)(uintptr_t)src, &u);
+  r = copy_units(st, u, 0, s);
+  if (r != HS_OK) return r;
+  return end_call(st, s);
+  ABI_END
+}
+
+extern "C" hs_status hs_kv_export_head(const hs_stage* st, int32_t n, const int64_t* ids,
+                                       void* host_dst, uint64_t cap, uint64_t* written) {
+  ABI_BEGIN
+  if (!st || !written) return fail(HS_EINVAL, "null argument");
+  std::vector<BlobRecord> recs;
+  BlobHeader h;
+  hs_status r = export_records(st, n, ids, &recs, &h);
+  if (r != HS_OK) return r;
+  std::vector<uint8_t> head = blob_encode_head(h, recs);
+  *written = head.size();
+  if (cap < head.size()) return fail(HS_ERANGE, "destination smaller than the blob head");
+  if (!host_dst) return fail(HS_EINVAL, "null destination");
+  memcpy(host_dst, head.data(), head.size());
+  return HS_OK;
+  ABI_END
+}
+
+extern "C" hs_status hs_kv_import_many(hs_stage* st, int32_t n_blobs, const void* const* srcs,
+                                       const uint64_t* bytes, const void* const* heads,
+                                       const uint64_t* head_bytes, void* stream) {
+  ABI_BEGIN
+  if (!st || n_blobs < 1 || !srcs || !bytes || !heads || !head_bytes)
+    return fail(HS_EINVAL, "bad arguments");
+  DeviceGuard dg(st->device);
+  for (int i = 0; i < n_blobs; ++i) {
+    if (!srcs[i] || !heads[i]) return fail(HS_EINVAL, "null blob or head");
+    if (!is_device_ptr(srcs[i])) return fail(HS_EINVAL, "blob source must be device memory");
+    if ((uintptr_t)srcs[i] & 15) return fail(HS_EINVAL, "blob source must be 16-byte aligned");
+  }
+  // every blob is checked against the state the blobs before it leave, on
+  // copies of the sequence table and free list; the stage changes only once
+  // all of them pass and the copy descriptors are reserved
+  SeqTable seqs = st->seqs;
+  std::vector<int32_t> free_blocks = st->free_blocks;
+  std::vector<BlobHeader> hs_(n_blobs);
+  std::vector<std::vector<BlobRecord>> recs(n_blobs);
+  uint64_t units = 0;
+  for (int i = 0; i < n_blobs; ++i) {
+    hs_status r = import_check(st, seqs, free_blocks.size(),
+                               static_cast<const uint8_t*>(heads[i]), head_bytes[i], bytes[i],
+                               &hs_[i], &recs[i]);
+    if (r != HS_OK) return fail(r, "blob " + std::to_string(i) + ": " + hs_last_error());
+    import_commit(seqs, free_blocks, hs_[i], recs[i]);
+    units += import_unit_count(hs_[i], recs[i]);
+  }
+  hs_status r = desc_reserve(st, units + 1);  // the last step that can fail
+  if (r != HS_OK) return r;
+  hipStream_t s = pick(st, stream);
+  r = begin_call(st, s);
+  if (r != HS_OK) return r;
+  st->seqs.swap(seqs);
+  st->free_blocks.swap(free_blocks);
+  Units u;
+  for (int i = 0; i < n_blobs; ++i)
+    import_units(st, st->seqs, hs_[i], recs[i], (uint64_t)(uintptr_t)srcs[i], &u);
   r = copy_units(st, u, 0, s);
   if (r != HS_OK) return r;
   return end_call(st, s);
@@ -1466,12 +1535,14 @@ extern "C" hs_status hs_kv_import_host(hs_stage* st, const void* src, uint64_t b
   if (r != HS_OK) return r;
   BlobHeader h;
   std::vector<BlobRecord> recs;
-  r = import_check(st, hb, kBlobHeader + kBlobRecord * (uint64_t)ns, bytes, &h, &recs);
+  r = import_check(st, st->seqs, st->free_blocks.size(), hb,
+                   kBlobHeader + kBlobRecord * (uint64_t)ns, bytes, &h, &recs);
   if (r != HS_OK) return r;
   r = desc_reserve(st, import_unit_count(h, recs) + 1);  // the last step that can fail
   if (r != HS_OK) return r;
-  import_commit(st, h, recs);
-  Units u = import_units(st, h, recs, (uint64_t)(uintptr_t)st->d_stage);
+  import_commit(st->seqs, st->free_blocks, h, recs);
+  Units u;
+  import_units(st, st->seqs, h, recs, (uint64_t)(uintptr_t)st->d_stage, &u);
   r = begin_call(st, s);
   if (r != HS_OK) return r;
   xfer_reset(st);

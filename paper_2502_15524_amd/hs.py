@@ -97,6 +97,10 @@ _SIGS = {
     "hs_kv_export": [_P, C.c_int32, C.POINTER(C.c_int64), _P, C.c_uint64,
                      C.POINTER(C.c_uint64), _P],
     "hs_kv_import": [_P, _P, C.c_uint64, _P],
+    "hs_kv_export_head": [_P, C.c_int32, C.POINTER(C.c_int64), _P, C.c_uint64,
+                          C.POINTER(C.c_uint64)],
+    "hs_kv_import_many": [_P, C.c_int32, C.POINTER(_P), C.POINTER(C.c_uint64), C.POINTER(_P),
+                          C.POINTER(C.c_uint64), _P],
     "hs_kv_export_host": [_P, C.c_int32, C.POINTER(C.c_int64), _P, C.c_uint64, C.c_uint64,
                           C.POINTER(C.c_uint64), _P],
     "hs_kv_import_host": [_P, _P, C.c_uint64, C.c_uint64, _P],
@@ -297,6 +301,31 @@ def hs_kv_export(h, seq_ids, dst_ptr, cap, stream=0):
 
 def hs_kv_import(h, src_ptr, nbytes, stream=0):
     _check(lib().hs_kv_import(h, src_ptr, nbytes, stream or None))
+
+
+def hs_kv_export_head(h, seq_ids):
+    """The header + records (+ padding) of the blob hs_kv_export would write
+    for these sequences, as bytes (host)."""
+    ids, n = _i64(seq_ids)
+    w = C.c_uint64(0)
+    code = lib().hs_kv_export_head(h, n, ids, None, 0, C.byref(w))
+    if code != HS_ERANGE:
+        _check(code)
+    buf = C.create_string_buffer(w.value)
+    _check(lib().hs_kv_export_head(h, n, ids, buf, w.value, C.byref(w)))
+    return buf.raw[:w.value]
+
+
+def hs_kv_import_many(h, blobs, stream=0):
+    """blobs: list of (device pointer, size, head bytes) imported in one
+    launch, in order."""
+    n = len(blobs)
+    srcs = (C.c_void_p * n)(*[b[0] for b in blobs])
+    sizes = (C.c_uint64 * n)(*[b[1] for b in blobs])
+    keep = [C.create_string_buffer(bytes(b[2]), len(b[2])) for b in blobs]
+    heads = (C.c_void_p * n)(*[C.addressof(k) for k in keep])
+    hlen = (C.c_uint64 * n)(*[len(b[2]) for b in blobs])
+    _check(lib().hs_kv_import_many(h, n, srcs, sizes, heads, hlen, stream or None))
 
 
 def hs_kv_export_host(h, seq_ids, host_dst, cap, chunk_bytes=64 << 20, stream=0):

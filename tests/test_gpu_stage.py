@@ -308,6 +308,54 @@ def test_merge_equals_pipeline_bitwise(env):
                                  np.concatenate([lb, res[1][:, 0]]))
 
 
+def test_import_many_equals_one_stage_and_decodes_bitwise(env):
+    """The two one-layer stages' blobs of a sequence, imported in one call
+    (hs_kv_import_many, headers handed over on the host) into a fresh
+    two-layer stage: its export equals that of a two-layer stage that ran
+    the prefill itself, byte for byte, and it decodes exactly like the
+    pipeline. A bad blob anywhere in the list changes nothing."""
+    torch = G.torch()
+    hs = env["hs"]
+    sp = G.stream_ptr()
+    s0, s1 = make(env, 0, 1), make(env, 1, 2)
+    toks, _ = run_greedy([s0, s1], env["prompt"], 1, seq_id=3)
+    full = make(env, 0, 2)
+    run_greedy([full], env["prompt"], 1, seq_id=3)
+    blobs = []
+    for st in (s0, s1):
+        b = _export(st, [3])
+        head = hs.hs_kv_export_head(st.h, [3])
+        assert bytes(b[:len(head)].cpu().numpy().tobytes()) == head
+        blobs.append((b, head))
+    tgt = make(env, 0, 2)
+    before = tgt.info()
+    bad = blobs[1][0].clone()
+    with pytest.raises(hs.HSError) as e:      # second blob's length disagrees with its head
+        hs.hs_kv_import_many(tgt.h, [(blobs[0][0].data_ptr(), blobs[0][0].numel(), blobs[0][1]),
+                                     (bad.data_ptr(), bad.numel() - 16, blobs[1][1])], sp)
+    assert e.value.code == hs.HS_EINVAL and tgt.info() == before
+    hs.hs_kv_import_many(tgt.h, [(b.data_ptr(), b.numel(), hd) for b, hd in blobs], sp)
+    assert tgt.info()["live_seqs"] == 1 and hs.hs_seq_tokens(tgt.h, 3) == len(env["prompt"]) + 1
+    assert _export(tgt, [3]).cpu().numpy().tobytes() == _export(full, [3]).cpu().numpy().tobytes()
+    outs = []
+    for stages in ([s0, s1], [tgt]):
+        nxt = torch.tensor([int(toks[-1])], dtype=torch.int32, device="cuda")
+        lg = torch.zeros((1, CFG.vocab), dtype=torch.float32, device="cuda")
+        seq = []
+        for _ in range(3):
+            x = nxt.clone()
+            for st in stages:
+                if st.end == CFG.n_layers:
+                    st.decode([3], x.data_ptr(), nxt.data_ptr(), lg.data_ptr(), sp)
+                else:
+                    o = torch.zeros((1, CFG.hidden), dtype=torch.bfloat16, device="cuda")
+                    st.decode([3], x.data_ptr(), o.data_ptr(), 0, sp)
+                    x = o
+            seq.append(lg.cpu().numpy().copy())
+        outs.append(np.stack(seq))
+    assert np.array_equal(outs[0], outs[1])
+
+
 def test_chunk_order_does_not_change_results(env):
     torch = G.torch()
     img = env["imgs"][(0, 2)]
