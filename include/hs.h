@@ -57,7 +57,8 @@ typedef enum {
  * n_kv_heads KV heads (query head h reads KV head h / (n_heads/n_kv_heads)),
  * SwiGLU FFN of width ffn, no biases, untied LM head. head_dim must be 64
  * or 128, n_heads / n_kv_heads 1, 2 or 4; hidden a multiple of 64 (at most
- * 8192), ffn and vocab multiples of 16. */
+ * 8192), ffn and vocab multiples of 16 (at most 131072 and 1048576),
+ * n_layers at most 1024. */
 typedef struct {
   int32_t n_layers, hidden, n_heads, n_kv_heads, head_dim, ffn, vocab;
   float rms_eps, rope_base;

@@ -23,7 +23,7 @@ bool cfg_valid(const hs_model_cfg* c, std::string* why) {
     return false;
   };
   if (!c) return no("null model cfg");
-  if (c->n_layers <= 0) return no("n_layers must be positive");
+  if (c->n_layers <= 0 || c->n_layers > 1024) return no("n_layers must be in 1..1024");
   if (c->hidden <= 0 || c->hidden % 64) return no("hidden must be a positive multiple of 64");
   if (c->hidden > 8192) return no("hidden above 8192 is not supported");
   if (c->head_dim != 64 && c->head_dim != 128) return no("head_dim must be 64 or 128");
@@ -31,8 +31,10 @@ bool cfg_valid(const hs_model_cfg* c, std::string* why) {
     return no("n_heads must be a positive multiple of n_kv_heads");
   const int g = c->n_heads / c->n_kv_heads;
   if (g != 1 && g != 2 && g != 4) return no("n_heads / n_kv_heads must be 1, 2 or 4");
-  if (c->ffn <= 0 || c->ffn % 16) return no("ffn must be a positive multiple of 16");
-  if (c->vocab <= 0 || c->vocab % 16) return no("vocab must be a positive multiple of 16");
+  if (c->ffn <= 0 || c->ffn % 16 || c->ffn > (1 << 17))
+    return no("ffn must be a positive multiple of 16, at most 131072");
+  if (c->vocab <= 0 || c->vocab % 16 || c->vocab > (1 << 20))
+    return no("vocab must be a positive multiple of 16, at most 1048576");
   if (!(c->rms_eps > 0.f)) return no("rms_eps must be positive");
   if (!(c->rope_base > 1.f)) return no("rope_base must be above 1");
   return true;
@@ -180,9 +182,19 @@ hs_status blob_decode_head(const void* pv, uint64_t avail, BlobHeader* h,
     r[i].n_tokens = rd<int32_t>(p, o + 8);
     r[i].n_blocks = rd<int32_t>(p, o + 12);
     if (r[i].n_tokens <= 0) return fail(HS_EINVAL, "blob record with no tokens");
-    if (r[i].n_blocks != (r[i].n_tokens + x.block_size - 1) / x.block_size)
+    if ((int64_t)r[i].n_blocks != ((int64_t)r[i].n_tokens + x.block_size - 1) / x.block_size)
       return fail(HS_EINVAL, "blob record block count does not match its token count");
     if (!ids.insert(r[i].seq_id).second) return fail(HS_EINVAL, "blob repeats a sequence id");
+  }
+  // the payload must be representable: layers x blocks x unit bytes below
+  // 2^62 (computed without wrapping), before blob_sizes forms it in 64 bits
+  {
+    unsigned __int128 blocks = 0;
+    for (const BlobRecord& rc : r) blocks += (uint64_t)rc.n_blocks;
+    const unsigned __int128 pay = (unsigned __int128)(uint64_t)(x.layer_end - x.layer_begin) *
+                                  blocks *
+                                  blob_unit_bytes(x.n_kv_heads, x.head_dim, x.block_size);
+    if (pay >> 62) return fail(HS_EINVAL, "blob payload size out of range");
   }
   BlobHeader want = x;
   blob_sizes(&want, r);
