@@ -69,6 +69,9 @@ def parse():
     ap.add_argument("--traffic-probe", action="store_true",
                     help="only run a few warm prefill steps and a 256 MiB device copy "
                          "(the workload for hardware-counter passes)")
+    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="summarise two rocprofv3 counter passes over a --traffic-probe run "
+                         "(no GPU work)")
     ap.add_argument("--no-extras", action="store_true",
                     help="headline workload only")
     ap.add_argument("--extras", default=",".join(EXTRAS),
@@ -192,6 +195,8 @@ def cpu_baseline(wl, x_f32, stage_range, min_seconds=12.0):
 
 def main():
     args = parse()
+    if args.summarize_counters:
+        return summarize_counters(*args.summarize_counters, workload=args.workload)
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the stage engine "
               "has no multi-GPU path in this build", file=sys.stderr)
@@ -293,14 +298,23 @@ def bench_c2(args):
         st.sync()
         for _ in range(3):
             hs.hs_seq_free(st.h, prefill_once())
-        stream.synchronize()
-        src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
-        dstc = torch.empty_like(src)
-        src.fill_(1)
+        i = prefill_once()
+        od = torch.empty((1, H), dtype=torch.bfloat16, device=dev)
+        for k in range(4):
+            st.decode([i], xdec[k:k + 1].data_ptr(), od.data_ptr(), 0, sp)
+        size = hs.hs_kv_export_size(st.h, [i])
+        blob = torch.empty(size, dtype=torch.uint8, device=dev)
+        head = hs.hs_kv_export_head(st.h, [i])
+        dst = pipeline.Stage(cfg, b, e, max_seqs=4, max_ctx=max_ctx, max_batch_tokens=P)
         for _ in range(2):
-            dstc.copy_(src)
-        torch.cuda.synchronize()
-        log("[bench] traffic probe done: 3 prefill steps, 2 copies of 268435456 bytes")
+            hs.hs_kv_export(st.h, [i], blob.data_ptr(), size, sp)
+            hs.hs_kv_import_many(dst.h, [(blob.data_ptr(), size, head)], sp)
+            stream.synchronize()
+            hs.hs_seq_free(dst.h, i)
+        dst.close()
+        traffic_calibration_copies(torch, dev)
+        log("[bench] traffic probe done: 3 prefill steps, 4 decode steps, 2 KV exports and "
+            "imports, 2 copies of 268435456 bytes")
         st.close()
         return None
 
@@ -408,7 +422,7 @@ def bench_c2(args):
     roofline = {"bound": "mfma", "kernel": dom["name"],
                 "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": traffic_from_profiles(dom["name"]),
+                "traffic": traffic_from_profiles(dom["name"], wl.name),
                 "flops_per_launch": dom_flops, "avg_launch_us": round(dom_avg_s * 1e6, 2)}
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
@@ -515,7 +529,7 @@ def bench_c2(args):
         "decode_ms_per_step": round(dec_ms, 4),
         "decode_tok_s": round(1e3 / dec_ms, 1),
         "decode_hbm_frac": round(dec_bytes / (dec_ms / 1e3) / 1e9 / PEAK_HBM_GBPS, 4),
-        "decode_roofline": hbm_roofline(dstats, "decode"),
+        "decode_roofline": hbm_roofline(dstats, wl.name),
         "kv_export_GBps": round(2 * used / (exp_ms / 1e3) / 1e9, 1),
         "kv_import_GBps": round(2 * used / (imp_ms / 1e3) / 1e9, 1),
         "kv_import_with_readback_GBps": round(2 * used / (statistics.median(imp1) / 1e3) / 1e9, 1),
@@ -616,6 +630,8 @@ def bench_pipeline(wl, args, n_dec=None, oracle_sample=False):
     hid = [torch.empty((T, H), dtype=torch.bfloat16, device=dev) for _ in range(2)]
     nxt = torch.empty(B, dtype=torch.int32, device=dev)
     ids_next = [10_000]
+    if args.traffic_probe:
+        return pipeline_probe(wl, args, stages, toks, hid, nxt, lens, max_ctx, stream)
 
     def prefill_all():
         ids = list(range(ids_next[0], ids_next[0] + B))
@@ -834,7 +850,7 @@ def bench_pipeline(wl, args, n_dec=None, oracle_sample=False):
                      "merged_decode_tok_s": round(B / ms_dec_m * 1e3, 1),
                      "merged_decode_hbm_frac": round(dec_bytes_m / (ms_dec_m / 1e3) / 1e9 /
                                                      PEAK_HBM_GBPS, 4),
-                     "merged_decode_roofline": hbm_roofline(mstats, wl.name + ":merged")}
+                     "merged_decode_roofline": hbm_roofline(mstats, wl.name)}
     res = {
         "metric": METRIC, "value": round(T / ms_pre * 1e3, 1), "unit": "tok/s", "n_gpus": 1,
         "steps": reps, "warmup": 1, "ms_per_step": round(ms_pre, 4), "higher_is_better": True,
@@ -860,6 +876,149 @@ def bench_pipeline(wl, args, n_dec=None, oracle_sample=False):
     if oracle_sample:
         res["cpu_baseline"] = oracle_sample_pipeline(wl, T, B, lens, moved if merge else 0)
     return res
+
+
+def traffic_calibration_copies(torch, dev):
+    """Two device copies of 256 MiB: the known-size dispatches that scale
+    the FETCH_SIZE / WRITE_SIZE counters of a probe run."""
+    src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+    dstc = torch.empty_like(src)
+    src.fill_(1)
+    for _ in range(2):
+        dstc.copy_(src)
+    torch.cuda.synchronize()
+
+
+def pipeline_probe(wl, args, stages, toks, hid, nxt, lens, max_ctx, stream):
+    """Workload for hardware-counter passes of a whole pipeline: one prefill,
+    4 decode steps, and for a merge workload one export per stage and one
+    import of all blobs; then the calibration copies."""
+    import torch
+    from paper_2502_15524_amd import hs, pipeline
+    cfg = wl.cfg
+    B, T, H = len(lens), sum(lens), cfg.hidden
+    sp = stream.cuda_stream
+    ids = list(range(B))
+    x = toks
+    for i, st in enumerate(stages):
+        out = nxt if i == len(stages) - 1 else hid[i % 2]
+        st.prefill(ids, lens, x.data_ptr(), out.data_ptr(), 0, sp)
+        x = out
+    tok = [nxt.clone(), torch.empty_like(nxt)]
+    hb = [torch.empty((B, H), dtype=torch.bfloat16, device=nxt.device) for _ in range(2)]
+    for k in range(4):
+        x = tok[k % 2]
+        for i, st in enumerate(stages):
+            out = tok[(k + 1) % 2] if i == len(stages) - 1 else hb[i % 2]
+            st.decode(ids, x.data_ptr(), out.data_ptr(), 0, sp)
+            x = out
+    what = "1 prefill, 4 decode steps"
+    if wl.name.endswith("merge"):
+        many = []
+        for st in stages:
+            n = hs.hs_kv_export_size(st.h, ids)
+            blob = torch.empty(n, dtype=torch.uint8, device=nxt.device)
+            hs.hs_kv_export(st.h, ids, blob.data_ptr(), n, sp)
+            many.append((blob, n, hs.hs_kv_export_head(st.h, ids)))
+        tgt = pipeline.Stage(cfg, 0, cfg.n_layers, max_seqs=B + 2, max_ctx=max_ctx,
+                             max_batch_tokens=T)
+        hs.hs_kv_import_many(tgt.h, [(b.data_ptr(), n, hd) for b, n, hd in many], sp)
+        stream.synchronize()
+        tgt.close()
+        what += f", {len(stages)} KV exports and one import of all of them"
+    stream.synchronize()
+    for st in stages:
+        st.close()
+    traffic_calibration_copies(torch, nxt.device)
+    log(f"[bench] traffic probe done ({wl.name}): {what}, 2 copies of 268435456 bytes")
+    return None
+
+
+_EPI_NAMES = ["store", "resid", "swiglu", "f32", "qkv_rope"]
+
+
+def bench_kernel_name(rocprof_name):
+    """The launch name bench.py reports (LaunchInfo) for a rocprofv3 kernel
+    name, and the source file of the kernel; (None, None) for others."""
+    import re
+    m = re.search(r"gemm_ring<(\d+), (\d+), \d+, \d+, (true|false), (\d+)>", rocprof_name)
+    if m:
+        sk = "sk" if m.group(3) == "true" else ""
+        return f"gemm_r{m.group(1)}x{m.group(2)}{sk}_{_EPI_NAMES[int(m.group(4))]}", "k_gemm"
+    m = re.search(r"gemm_skinny<\d+, \d+, \d+, (\d+), (true|false), \d+>", rocprof_name)
+    if m:
+        norm = "norm_" if m.group(2) == "true" else ""
+        return f"gemm_skinny_{norm}{_EPI_NAMES[int(m.group(1))]}", "k_gemm"
+    m = re.search(r"attn_prefill_kernel<(\d+),", rocprof_name)
+    if m:
+        return f"attn_prefill_d{m.group(1)}", "k_attn"
+    if "attn_decode" in rocprof_name:
+        return "attn_decode", "k_attn"
+    for k in ("kv_copy", "rmsnorm", "embed", "argmax", "rope_kv"):
+        if k + "_kernel" in rocprof_name or (k == "argmax" and "argmax" in rocprof_name):
+            return k, "k_misc"
+    return None, None
+
+
+def summarize_counters(fetch_csv, write_csv, workload):
+    """Per-kernel HBM traffic of a probe run from two rocprofv3 counter
+    passes (FETCH_SIZE, WRITE_SIZE; KiB per dispatch), each scaled by what it
+    reads for the two 256 MiB calibration copies at the end of the run.
+    Prints a markdown table and the machine-readable "traffic:" lines that
+    traffic_from_profiles() reads."""
+    import csv
+    from collections import defaultdict
+
+    def load(path):
+        rows = list(csv.DictReader(open(path)))
+        rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+        return rows
+    f_rows, w_rows = load(fetch_csv), load(write_csv)
+    copy_f = [float(r["Counter_Value"]) for r in f_rows if "copy" in r["Kernel_Name"].lower()][-2:]
+    copy_w = [float(r["Counter_Value"]) for r in w_rows if "copy" in r["Kernel_Name"].lower()][-2:]
+    kib = 268435456 / 1024
+    sf, sw = kib / (sum(copy_f) / 2), kib / (sum(copy_w) / 2)
+    per = defaultdict(lambda: [0, 0.0, 0.0])
+    for rows, idx in ((f_rows, 1), (w_rows, 2)):
+        for r in rows:
+            per[r["Kernel_Name"]][idx] += float(r["Counter_Value"])
+            if idx == 1:
+                per[r["Kernel_Name"]][0] += 1
+    csrc = os.path.join(ROOT, "paper_2502_15524_amd", "csrc")
+    print(f"calibration: FETCH_SIZE x{sf:.3f}, WRITE_SIZE x{sw:.3f} (two copies of 268435456 B)")
+    print("| kernel (rocprofv3 name) | bench name | dispatches | FETCH_SIZE KiB / dispatch | "
+          "WRITE_SIZE KiB / dispatch | calibrated HBM bytes / dispatch |")
+    print("|---|---|---|---|---|---|")
+    lines, attn = [], 0.0
+    owners = defaultdict(set)        # bench name -> rocprofv3 kernels behind it
+    for name in per:
+        owners[bench_kernel_name(name)[0]].add(name)
+    for name, (n, f, w) in sorted(per.items(), key=lambda kv: -(kv[1][1] + kv[1][2])):
+        bname, src = bench_kernel_name(name)
+        if not bname or n == 0:
+            continue
+        fb, wb = f / n, w / n
+        hbm = (fb * sf + wb * sw) * 1024
+        short = name.split("(")[0].replace("void ", "")
+        print(f"| `{short}` | {bname} | {n} | {fb:,.1f} | {wb:,.1f} | {hbm:,.0f} |")
+        if bname == "attn_decode":
+            attn += hbm   # split + combine kernels form one call
+            src_attn = src
+            continue
+        if bname == "kv_copy" and workload.endswith("merge"):
+            # the probe's copies are one export of every stage and one import
+            # of all blobs: two operations of equal size
+            hbm = (f * sf + w * sw) * 1024 / 2
+        elif len(owners[bname]) > 1:
+            continue      # two launch sites share the name (o and down): no line
+        lines.append(f"traffic: kernel={bname} workload={workload} hbm_bytes_per_launch="
+                     f"{int(hbm)} {src}_sha256={_sha(os.path.join(csrc, src + '.hip'))}")
+    if attn:
+        lines.append(f"traffic: kernel=attn_decode workload={workload} hbm_bytes_per_launch="
+                     f"{int(attn)} {src_attn}_sha256={_sha(os.path.join(csrc, src_attn + '.hip'))}")
+    print()
+    for l in lines:
+        print(l)
 
 
 def oracle_sample_pipeline(wl, T, B, lens, kv_bytes):
