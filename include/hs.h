@@ -191,6 +191,13 @@ hs_status hs_stage_sync(hs_stage* st);
  * its weights land while later chunks are still in flight.
  * `pinned_src` must be page-locked (hipHostMalloc) and stay valid until the
  * chunk has landed (hs_stage_loaded or hs_stage_sync).
+ * Overlap needs the copy streams on hardware queues of their own: HIP
+ * spreads a process's streams over GPU_MAX_HW_QUEUES queues (4 by
+ * default) and runs one queue's work in order, so a prefill whose stream
+ * shares a queue with a copy stream starts only after every chunk queued
+ * there. Set GPU_MAX_HW_QUEUES, before the HIP runtime starts, to at least
+ * the number of streams in use (the stage's copy streams, the caller's
+ * streams); 8 suffices for one loading stage and a few caller streams.
  * Errors: HS_EINVAL (range outside the image, overlap, NULL src), HS_EHIP. */
 hs_status hs_stage_load_chunk(hs_stage* st, uint64_t image_offset,
                               const void* pinned_src, uint64_t bytes);
