@@ -351,9 +351,9 @@ hs_status hs_kv_import_many(hs_stage* st, int32_t n_blobs, const void* const* sr
  * also carries the header and records).
  *
  * hs_kv_export_host: like hs_kv_export, but `dst` is pinned host memory
- * (hipHostMalloc). The blocks are gathered chunk by chunk into a device
+ * (hs_host_alloc). The blocks are gathered chunk by chunk into a device
  * staging buffer owned by the stage (grown on demand) and every chunk is
- * copied to `dst` on the stage's copy streams as soon as it is gathered.
+ * copied to `dst` on `stream` as soon as it is gathered.
  * hs_kv_host_progress reports the landed prefix without blocking; the call
  * as a whole is complete (ordered on `stream` and for later calls) when
  * every chunk has landed.
@@ -427,6 +427,15 @@ hs_status hs_stage_read_timing(hs_stage* st, hs_kernel_stat* out, int32_t cap,
 
 /* Thread-local description of the last error (never NULL). */
 const char* hs_last_error(void);
+
+/* Page-locked host memory (hipHostMalloc) from the HIP runtime the library
+ * itself uses, for weight images (hs_stage_load_chunk) and host-staged KV
+ * blobs. Memory the GPU copies from or to must be known to that runtime as
+ * page-locked: a buffer locked by another runtime instance in the process
+ * is copied through staging buffers, at a fraction of the host-link rate.
+ * hs_host_free(NULL) is a no-op. Errors: HS_EINVAL (null out), HS_ENOMEM. */
+hs_status hs_host_alloc(uint64_t bytes, void** out);
+hs_status hs_host_free(void* p);
 
 #ifdef __cplusplus
 }

@@ -97,6 +97,8 @@ _SIGS = {
     "hs_kv_export": [_P, C.c_int32, C.POINTER(C.c_int64), _P, C.c_uint64,
                      C.POINTER(C.c_uint64), _P],
     "hs_kv_import": [_P, _P, C.c_uint64, _P],
+    "hs_host_alloc": [C.c_uint64, C.POINTER(_P)],
+    "hs_host_free": [_P],
     "hs_kv_export_head": [_P, C.c_int32, C.POINTER(C.c_int64), _P, C.c_uint64,
                           C.POINTER(C.c_uint64)],
     "hs_kv_import_many": [_P, C.c_int32, C.POINTER(_P), C.POINTER(C.c_uint64), C.POINTER(_P),
@@ -301,6 +303,18 @@ def hs_kv_export(h, seq_ids, dst_ptr, cap, stream=0):
 
 def hs_kv_import(h, src_ptr, nbytes, stream=0):
     _check(lib().hs_kv_import(h, src_ptr, nbytes, stream or None))
+
+
+def hs_host_alloc(nbytes):
+    """Page-locked host memory from the library's HIP runtime; returns the
+    address (free it with hs_host_free)."""
+    p = C.c_void_p()
+    _check(lib().hs_host_alloc(nbytes, C.byref(p)))
+    return p.value
+
+
+def hs_host_free(ptr):
+    _check(lib().hs_host_free(ptr))
 
 
 def hs_kv_export_head(h, seq_ids):

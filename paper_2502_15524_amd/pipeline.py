@@ -60,40 +60,28 @@ def pack_image(cfg, rb, re, image_ptr, source=None, threads=8):
 
 
 class PinnedBuffer:
-    """Page-locked host memory from hipHostMalloc, released on close() or
-    garbage collection (not cached). Exposes data_ptr() and numel() (bytes)."""
-
-    _hip = None
+    """Page-locked host memory from the library (hs_host_alloc, i.e.
+    hipHostMalloc in the HIP runtime the library and torch share), released
+    on close() or garbage collection (not cached). Exposes data_ptr() and
+    numel() (bytes)."""
 
     def __init__(self, nbytes):
-        import ctypes
-        if PinnedBuffer._hip is None:
-            lib = ctypes.CDLL("libamdhip64.so")
-            lib.hipHostMalloc.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_size_t,
-                                          ctypes.c_uint]
-            lib.hipHostMalloc.restype = ctypes.c_int
-            lib.hipHostFree.argtypes = [ctypes.c_void_p]
-            lib.hipHostFree.restype = ctypes.c_int
-            PinnedBuffer._hip = lib
-        self._p = ctypes.c_void_p()
-        rc = PinnedBuffer._hip.hipHostMalloc(ctypes.byref(self._p), nbytes, 0)
-        if rc != 0 or not self._p.value:
-            raise MemoryError(f"hipHostMalloc({nbytes}) failed with {rc}")
+        self._p = hs.hs_host_alloc(nbytes)
         self._n = nbytes
 
     def data_ptr(self):
-        return self._p.value
+        return self._p
 
     def numel(self):
         return self._n
 
     def numpy(self):
         import ctypes
-        return np.ctypeslib.as_array((ctypes.c_uint8 * self._n).from_address(self._p.value))
+        return np.ctypeslib.as_array((ctypes.c_uint8 * self._n).from_address(self._p))
 
     def close(self):
-        if self._p is not None and self._p.value:
-            PinnedBuffer._hip.hipHostFree(self._p)
+        if self._p:
+            hs.hs_host_free(self._p)
             self._p = None
 
     def __del__(self):
