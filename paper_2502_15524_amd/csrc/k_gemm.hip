@@ -14,7 +14,7 @@
 //
 // Two kernels:
 //  * gemm_ring   - prefill: BN x BM x 64 tiles copied straight into an LDS ring
-//                  of NS stages, 4 waves, 16x16x32 bf16 MFMA, XCD-aware order.
+//                  of NS stages, 8 waves, 16x16x32 bf16 MFMA, XCD-aware order.
 //  * gemm_skinny - decode (M <= 64 tokens): HBM-bound weight streaming, 2,
 //                  4 or 8 waves split K inside a workgroup, reduced through
 //                  LDS in a fixed order (deterministic).
@@ -178,16 +178,19 @@ __device__ __forceinline__ void wait_vm() {
 
 __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
-template <int BN, int BM, int BK, int NS>
+// NW waves per workgroup as 2 x NW/2: two wave columns over the BN weight
+// rows, NW/2 wave rows over the BM tokens.
+template <int BN, int BM, int BK, int NS, int NW = 4>
 struct RTile {
   static constexpr int CPR = BK / 8;           // 16-byte chunks per row
   static constexpr int RPI = 64 / CPR;         // rows per load instruction
-  static constexpr int WN = BN / 2, WM = BM / 2, TN = WN / 16, TM = WM / 16;
-  static constexpr int WI = BN / 4 / RPI, XI = BM / 4 / RPI;  // instructions per wave
+  static constexpr int WN = BN / 2, WM = BM / (NW / 2), TN = WN / 16, TM = WM / 16;
+  static constexpr int WI = BN / NW / RPI, XI = BM / NW / RPI;  // instructions per wave
   static constexpr int LPS = WI + XI;          // loads per stage per wave
   static constexpr int W_BYTES = BN * BK * 2, STAGE = (BN + BM) * BK * 2;
   static_assert(BK == 64, "weights come in 64-column slabs");
-  static_assert(WI >= 1 && XI >= 1, "tile too small for 4 waves");
+  static_assert(NW == 4 || NW == 8, "4 or 8 waves");
+  static_assert(WI >= 1 && XI >= 1 && TM >= 1, "tile too small for the waves");
 };
 
 // position of chunk c of row r inside its row
@@ -209,12 +212,12 @@ __device__ __forceinline__ bf16x8_v lds_frag(const bf16_t* s, int r, int c) {
   return as_bf16x8(ld16(s + (r * CPR + chunk_pos<CPR>(r, c)) * 8));
 }
 
-template <int BN, int BM, int BK, int NS, int TN, int TM, typename Dma>
+template <int BN, int BM, int BK, int NS, int NW, int TN, int TM, typename Dma>
 __device__ __forceinline__ void ring_stage(f32x4_v (&acc)[TN][TM], bf16x8_v (&a)[2],
                                            bf16x8_v (&b)[2][TM], const bf16_t* sw,
                                            const bf16_t* sx, int wn, int wm, int fr, int g,
                                            bool pending, Dma&& dma) {
-  using T = RTile<BN, BM, BK, NS>;
+  using T = RTile<BN, BM, BK, NS, NW>;
   constexpr int CPR = T::CPR, KS = BK / 32;
   constexpr int MASK_MFMA = 0x008, MASK_DS_READ = 0x100;
   static_assert(TN % 2 == 0 && KS == 2, "the deferred row tile uses a[1] and b[1]");
@@ -290,11 +293,11 @@ __device__ __forceinline__ int sk_owner(int64_t i, int64_t total, int G) {
   return (int)(((i + 1) * G - 1) / total);
 }
 
-template <int BN, int BM, int NS, int SPR, bool SK, int EPI>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+template <int BN, int BM, int NS, int SPR, bool SK, int EPI, int NW = 4>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NW / 4, NW / 4)))
 void gemm_ring(GemmArgs a, GemmSched sc) {
   constexpr int BK = 64;
-  using T = RTile<BN, BM, BK, NS>;
+  using T = RTile<BN, BM, BK, NS, NW>;
   constexpr int CPR = T::CPR, RPI = T::RPI, WN = T::WN, WM = T::WM, TN = T::TN, TM = T::TM;
   constexpr int LPS = T::LPS;
   static_assert((EPI != EPI_SWIGLU && EPI != EPI_QKV_ROPE) || (WN % 32) == 0,
@@ -318,8 +321,8 @@ void gemm_ring(GemmArgs a, GemmSched sc) {
   const int sw_slab = (a.N / 8) * 1024;
   const int sx_step = RPI * (int)a.ldx * 2;
   const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) char*)smem;
-  const uint32_t lds_w = lds0 + wave_u * (BN / 4) * BK * 2;
-  const uint32_t lds_x = lds0 + T::W_BYTES + wave_u * (BM / 4) * BK * 2;
+  const uint32_t lds_w = lds0 + wave_u * (BN / NW) * BK * 2;
+  const uint32_t lds_x = lds0 + T::W_BYTES + wave_u * (BM / NW) * BK * 2;
   const int fr = lane & 15, g = lane >> 4;
 
   f32x4_v acc[TN][TM];
@@ -365,9 +368,9 @@ void gemm_ring(GemmArgs a, GemmSched sc) {
     for (int i = 0; i < TN; ++i)
 #pragma unroll
       for (int j = 0; j < TM; ++j) acc[i][j] = f32x4_v{0.f, 0.f, 0.f, 0.f};
-    // weights: block (kt, n0/8 + wave * BN/32 + q) of the tiled format
-    const int sw_base = (n0 / 8 + wave_u * (BN / 32)) * 1024;
-    const int vx = ((m0 + wave * (BM / 4) + lrow) * (int)a.ldx + lchunk * 8) * 2;
+    // weights: block (kt, n0/8 + wave * BN/(8 NW) + q) of the tiled format
+    const int sw_base = (n0 / 8 + wave_u * (BN / NW / 8)) * 1024;
+    const int vx = ((m0 + wave * (BM / NW) + lrow) * (int)a.ldx + lchunk * 8) * 2;
     auto issue_one = [&](int stage, int kt, int q) {
       const uint32_t so = stage * T::STAGE;
       if (q < T::WI) dma16(rw, vw, sw_base + kt * sw_slab + q * 1024, lds_w + so + q * 1024);
@@ -404,7 +407,7 @@ void gemm_ring(GemmArgs a, GemmSched sc) {
       const bool more = j + NS - 1 < n;
       const bf16_t* sw = reinterpret_cast<const bf16_t*>(smem + stage * T::STAGE);
       const bf16_t* sx = reinterpret_cast<const bf16_t*>(smem + stage * T::STAGE + T::W_BYTES);
-      ring_stage<BN, BM, BK, NS>(acc, fa, fb, sw, sx, wn, wm, fr, g, j > 0, [&](int step) {
+      ring_stage<BN, BM, BK, NS, NW>(acc, fa, fb, sw, sx, wn, wm, fr, g, j > 0, [&](int step) {
         if (more) issue_part(nst, kn, step);
       });
       if (more) wait_vm<(NS - 2) * LPS>();
@@ -477,7 +480,7 @@ void gemm_ring(GemmArgs a, GemmSched sc) {
   typedef unsigned u32x4_v __attribute__((ext_vector_type(4)));
   const __amdgpu_buffer_rsrc_t rp =
       __builtin_amdgcn_make_buffer_rsrc(a.part, 0, 0x7FFFFFFF, kRsrcWord3);
-  auto frag_off = [&](int i, int j) { return (((i * TM + j) * 4 + wave) * 64 + lane) * 16; };
+  auto frag_off = [&](int i, int j) { return (((i * TM + j) * NW + wave) * 64 + lane) * 16; };
   const int64_t beg = sk_begin(l, sc.total, G), end = sk_begin(l + 1, sc.total, G);
   for (int64_t it = beg; it < end;) {
     const int t = (int)(it / sc.nk);
@@ -791,14 +794,15 @@ hipError_t dispatch_skinny1(const GemmArgs& a, int epi, int nf, int u, int wv, h
   return hipErrorInvalidValue;
 }
 
-template <int BN, int BM, int NS, int SPR, bool SK>
+template <int BN, int BM, int NS, int SPR, bool SK, int NW = 4>
 hipError_t dispatch_ring(const GemmArgs& a, int epi, const GemmSched& sc, int grid, hipStream_t s) {
+  const dim3 blk(64 * NW);
   switch (epi) {
-    case EPI_STORE: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_STORE>), dim3(grid), dim3(256), 0, s, a, sc); break;
-    case EPI_RESID: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_RESID>), dim3(grid), dim3(256), 0, s, a, sc); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_SWIGLU>), dim3(grid), dim3(256), 0, s, a, sc); break;
-    case EPI_F32: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_F32>), dim3(grid), dim3(256), 0, s, a, sc); break;
-    case EPI_QKV_ROPE: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_QKV_ROPE>), dim3(grid), dim3(256), 0, s, a, sc); break;
+    case EPI_STORE: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_STORE, NW>), dim3(grid), blk, 0, s, a, sc); break;
+    case EPI_RESID: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_RESID, NW>), dim3(grid), blk, 0, s, a, sc); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_SWIGLU, NW>), dim3(grid), blk, 0, s, a, sc); break;
+    case EPI_F32: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_F32, NW>), dim3(grid), blk, 0, s, a, sc); break;
+    case EPI_QKV_ROPE: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_QKV_ROPE, NW>), dim3(grid), blk, 0, s, a, sc); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -819,14 +823,35 @@ const RingCfg kRing[] = {{"256x256", 256, 256, false}, {"256x128", 256, 128, tru
 // 192 x 128 (160 KiB) and 128 x 128: 4 stages.
 hipError_t launch_ring(const RingCfg& c, const GemmArgs& a, int epi, const GemmSched& sc,
                        int grid, hipStream_t s) {
-  if (c.bn == 256 && c.bm == 256) return dispatch_ring<256, 256, 2, 2, false>(a, epi, sc, grid, s);
-  if (c.bn == 192 && c.bm == 256) return dispatch_ring<192, 256, 2, 2, false>(a, epi, sc, grid, s);
-  if (c.bn == 192 && c.bm == 128) return dispatch_ring<192, 128, 4, 4, false>(a, epi, sc, grid, s);
-  if (c.bn == 256 && c.bm == 128)
-    return sc.sk ? dispatch_ring<256, 128, 3, 4, true>(a, epi, sc, grid, s)
-                 : dispatch_ring<256, 128, 3, 4, false>(a, epi, sc, grid, s);
-  return sc.sk ? dispatch_ring<128, 128, 4, 4, true>(a, epi, sc, grid, s)
-               : dispatch_ring<128, 128, 4, 4, false>(a, epi, sc, grid, s);
+  // Eight waves (two per SIMD: one wave's LDS reads and barrier waits hide
+  // behind the other's MFMAs) unless HS_GEMM_WAVES=4 (tuning only). The
+  // 512-token 7B stage, MI355X: o 36.5 -> 32.9 us, down 69.8 -> 65.5, QKV
+  // 66.7 -> 59.7, gate/up unchanged; 8192 tokens: o 240 -> 219, QKV 674 -> 647.
+  // Each output is still summed by one wave in k order, so the bits do not
+  // change.
+  static const char* waves = getenv("HS_GEMM_WAVES");
+  const bool w4 = waves && atoi(waves) == 4;
+  if (c.bn == 256 && c.bm == 256)
+    return w4 ? dispatch_ring<256, 256, 2, 2, false>(a, epi, sc, grid, s)
+              : dispatch_ring<256, 256, 2, 2, false, 8>(a, epi, sc, grid, s);
+  if (c.bn == 192 && c.bm == 256)
+    return w4 ? dispatch_ring<192, 256, 2, 2, false>(a, epi, sc, grid, s)
+              : dispatch_ring<192, 256, 2, 2, false, 8>(a, epi, sc, grid, s);
+  if (c.bn == 192 && c.bm == 128)
+    return w4 ? dispatch_ring<192, 128, 4, 4, false>(a, epi, sc, grid, s)
+              : dispatch_ring<192, 128, 4, 4, false, 8>(a, epi, sc, grid, s);
+  if (c.bn == 256 && c.bm == 128) {
+    if (w4)
+      return sc.sk ? dispatch_ring<256, 128, 3, 4, true>(a, epi, sc, grid, s)
+                   : dispatch_ring<256, 128, 3, 4, false>(a, epi, sc, grid, s);
+    return sc.sk ? dispatch_ring<256, 128, 3, 4, true, 8>(a, epi, sc, grid, s)
+                 : dispatch_ring<256, 128, 3, 4, false, 8>(a, epi, sc, grid, s);
+  }
+  if (w4)
+    return sc.sk ? dispatch_ring<128, 128, 4, 4, true>(a, epi, sc, grid, s)
+                 : dispatch_ring<128, 128, 4, 4, false>(a, epi, sc, grid, s);
+  return sc.sk ? dispatch_ring<128, 128, 4, 4, true, 8>(a, epi, sc, grid, s)
+               : dispatch_ring<128, 128, 4, 4, false, 8>(a, epi, sc, grid, s);
 }
 
 int device_cus() {
