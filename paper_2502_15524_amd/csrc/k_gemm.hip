@@ -293,16 +293,22 @@ __device__ __forceinline__ int sk_owner(int64_t i, int64_t total, int G) {
   return (int)(((i + 1) * G - 1) / total);
 }
 
-template <int BN, int BM, int NS, int SPR, bool SK, int EPI, int NW = 4>
+// NS weight stages and NSX activation stages (NSX = NS, or one more or one
+// fewer with two stages of the other): the loads of weight slab j + NS - 1
+// and activation slab j + NSX - 1 are in flight while slab j is multiplied.
+template <int BN, int BM, int NS, int SPR, bool SK, int EPI, int NW = 4, int NSX = NS>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NW / 4, NW / 4)))
 void gemm_ring(GemmArgs a, GemmSched sc) {
   constexpr int BK = 64;
   using T = RTile<BN, BM, BK, NS, NW>;
+  static_assert(NSX == NS || (NS == 2 && NSX == 3) || (NS == 3 && NSX == 2),
+                "stage counts: equal, or 2 and 3");
   constexpr int CPR = T::CPR, RPI = T::RPI, WN = T::WN, WM = T::WM, TN = T::TN, TM = T::TM;
   constexpr int LPS = T::LPS;
   static_assert((EPI != EPI_SWIGLU && EPI != EPI_QKV_ROPE) || (WN % 32) == 0,
                 "SwiGLU and RoPE need 32-row pairs");
-  __shared__ __attribute__((aligned(1024))) char smem[NS * T::STAGE];
+  constexpr int X_BYTES = BM * BK * 2;
+  __shared__ __attribute__((aligned(1024))) char smem[NS * T::W_BYTES + NSX * X_BYTES];
   __shared__ int s_last;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -321,8 +327,9 @@ void gemm_ring(GemmArgs a, GemmSched sc) {
   const int sw_slab = (a.N / 8) * 1024;
   const int sx_step = RPI * (int)a.ldx * 2;
   const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) char*)smem;
+  // weight stages first, then the activation stages
   const uint32_t lds_w = lds0 + wave_u * (BN / NW) * BK * 2;
-  const uint32_t lds_x = lds0 + T::W_BYTES + wave_u * (BM / NW) * BK * 2;
+  const uint32_t lds_x = lds0 + NS * T::W_BYTES + wave_u * (BM / NW) * BK * 2;
   const int fr = lane & 15, g = lane >> 4;
 
   f32x4_v acc[TN][TM];
@@ -371,47 +378,88 @@ void gemm_ring(GemmArgs a, GemmSched sc) {
     // weights: block (kt, n0/8 + wave * BN/(8 NW) + q) of the tiled format
     const int sw_base = (n0 / 8 + wave_u * (BN / NW / 8)) * 1024;
     const int vx = ((m0 + wave * (BM / NW) + lrow) * (int)a.ldx + lchunk * 8) * 2;
-    auto issue_one = [&](int stage, int kt, int q) {
-      const uint32_t so = stage * T::STAGE;
-      if (q < T::WI) dma16(rw, vw, sw_base + kt * sw_slab + q * 1024, lds_w + so + q * 1024);
-      else dma16(rx, vx, (q - T::WI) * sx_step + kt * BK * 2, lds_x + so + (q - T::WI) * 1024);
+    // load q of a step (0 <= q < LPS): the operand whose slab is due sooner
+    // goes first (weights when the look-aheads are equal)
+    constexpr int AW = NS - 1, AX = NSX - 1;          // look-ahead in steps
+    constexpr bool XFIRST = AX < AW;
+    constexpr int FIRST = XFIRST ? T::XI : T::WI, SECOND = LPS - FIRST;
+    auto issue_w = [&](int stage, int kt, int q) {
+      dma16(rw, vw, sw_base + kt * sw_slab + q * 1024, lds_w + stage * T::W_BYTES + q * 1024);
     };
-    // the loads of the next stage are spread over the first SPR/4 of the
-    // row-tile steps of the current stage's multiplication
+    auto issue_x = [&](int stage, int kt, int q) {
+      dma16(rx, vx, q * sx_step + kt * BK * 2, lds_x + stage * X_BYTES + q * 1024);
+    };
+    // the loads of a step are spread over the first SPR/4 of the row-tile
+    // steps of the current slab's multiplication
     constexpr int STEPS = TN * (BK / 32), USE = STEPS * SPR / 4;
     static_assert(USE >= 1, "spread");
-    auto issue_part = [&](int stage, int kt, int step) {
+    auto issue_part = [&](int j, int step, bool more_w, bool more_x) {
       if (step < USE) {
 #pragma unroll
-        for (int q = step * LPS / USE; q < (step + 1) * LPS / USE; ++q) issue_one(stage, kt, q);
+        for (int q = step * LPS / USE; q < (step + 1) * LPS / USE; ++q) {
+          const bool first = q < FIRST;
+          const bool is_x = first == XFIRST;
+          const int qq = first ? q : q - FIRST;
+          if (is_x) {
+            if (more_x) issue_x((j + AX) % NSX, k0 + j + AX, qq);
+          } else if (more_w) {
+            issue_w((j + AW) % NS, k0 + j + AW, qq);
+          }
+        }
       }
     };
-    // Step j issues the loads of step j + NS - 1 while it multiplies. The
-    // issue is behind a (uniform) branch on purpose: it splits the step into
-    // scheduling regions, without which the register allocator shuffles the
-    // accumulators between MFMAs.
+    // Step j issues the loads of weight slab j + AW and activation slab
+    // j + AX while it multiplies slab j. The issue is behind a (uniform)
+    // branch on purpose: it splits the step into scheduling regions, without
+    // which the register allocator shuffles the accumulators between MFMAs.
+    // Loads complete in issue order, so before slab j + 1 the wave waits
+    // until only the loads issued after slab j + 1's last one are
+    // outstanding: with equal look-aheads the (AW - 1) later steps' loads,
+    // else the second operand's loads of step j.
     const int n = k1 - k0;
+    // prologue: the loads of the virtual steps -max(AW, AX) .. -1, in the
+    // same order as the steady state
 #pragma unroll
-    for (int s = 0; s < NS - 1; ++s)
-      if (s < n) {
+    for (int v = -(AW > AX ? AW : AX); v < 0; ++v) {
+      const int tw = v + AW, tx = v + AX;   // slabs this virtual step loads
+      auto w_part = [&] {
+        if (tw >= 0 && tw < n)
 #pragma unroll
-        for (int q = 0; q < LPS; ++q) issue_one(s, k0 + s, q);
-      }
+          for (int q = 0; q < T::WI; ++q) issue_w(tw % NS, k0 + tw, q);
+      };
+      auto x_part = [&] {
+        if (tx >= 0 && tx < n)
+#pragma unroll
+          for (int q = 0; q < T::XI; ++q) issue_x(tx % NSX, k0 + tx, q);
+      };
+      if (XFIRST) { x_part(); w_part(); } else { w_part(); x_part(); }
+    }
     after_issue();
-    if (n >= NS - 1) wait_vm<(NS - 2) * LPS>();
-    else wait_vm<0>();
+    // before slab 0: what the prologue issued after slab 0's loads
+    if constexpr (AW == AX) {
+      if (n >= NS - 1) wait_vm<(NS - 2) * LPS>();
+      else wait_vm<0>();
+    } else {
+      if (n >= 2) wait_vm<SECOND>();
+      else wait_vm<0>();
+    }
     wg_barrier();
     bf16x8_v fa[2], fb[2][TM];
     for (int j = 0; j < n; ++j) {
-      const int stage = j % NS, nst = (j + NS - 1) % NS, kn = k0 + j + NS - 1;
-      const bool more = j + NS - 1 < n;
-      const bf16_t* sw = reinterpret_cast<const bf16_t*>(smem + stage * T::STAGE);
-      const bf16_t* sx = reinterpret_cast<const bf16_t*>(smem + stage * T::STAGE + T::W_BYTES);
+      const bool more_w = j + AW < n, more_x = j + AX < n;
+      const bf16_t* sw = reinterpret_cast<const bf16_t*>(smem + (j % NS) * T::W_BYTES);
+      const bf16_t* sx =
+          reinterpret_cast<const bf16_t*>(smem + NS * T::W_BYTES + (j % NSX) * X_BYTES);
       ring_stage<BN, BM, BK, NS, NW>(acc, fa, fb, sw, sx, wn, wm, fr, g, j > 0, [&](int step) {
-        if (more) issue_part(nst, kn, step);
+        issue_part(j, step, more_w, more_x);
       });
-      if (more) wait_vm<(NS - 2) * LPS>();
-      else wait_vm<0>();
+      if constexpr (AW == AX) {
+        if (more_w) wait_vm<(NS - 2) * LPS>();
+        else wait_vm<0>();
+      } else {
+        if (more_w && more_x) wait_vm<SECOND>();
+        else wait_vm<0>();
+      }
       wg_barrier();
     }
     // the last stage's deferred row tile
@@ -794,15 +842,15 @@ hipError_t dispatch_skinny1(const GemmArgs& a, int epi, int nf, int u, int wv, h
   return hipErrorInvalidValue;
 }
 
-template <int BN, int BM, int NS, int SPR, bool SK, int NW = 4>
+template <int BN, int BM, int NS, int SPR, bool SK, int NW = 4, int NSX = NS>
 hipError_t dispatch_ring(const GemmArgs& a, int epi, const GemmSched& sc, int grid, hipStream_t s) {
   const dim3 blk(64 * NW);
   switch (epi) {
-    case EPI_STORE: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_STORE, NW>), dim3(grid), blk, 0, s, a, sc); break;
-    case EPI_RESID: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_RESID, NW>), dim3(grid), blk, 0, s, a, sc); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_SWIGLU, NW>), dim3(grid), blk, 0, s, a, sc); break;
-    case EPI_F32: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_F32, NW>), dim3(grid), blk, 0, s, a, sc); break;
-    case EPI_QKV_ROPE: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_QKV_ROPE, NW>), dim3(grid), blk, 0, s, a, sc); break;
+    case EPI_STORE: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_STORE, NW, NSX>), dim3(grid), blk, 0, s, a, sc); break;
+    case EPI_RESID: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_RESID, NW, NSX>), dim3(grid), blk, 0, s, a, sc); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_SWIGLU, NW, NSX>), dim3(grid), blk, 0, s, a, sc); break;
+    case EPI_F32: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_F32, NW, NSX>), dim3(grid), blk, 0, s, a, sc); break;
+    case EPI_QKV_ROPE: hipLaunchKernelGGL((gemm_ring<BN, BM, NS, SPR, SK, EPI_QKV_ROPE, NW, NSX>), dim3(grid), blk, 0, s, a, sc); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -817,10 +865,10 @@ const RingCfg kRing[] = {{"256x256", 256, 256, false}, {"256x128", 256, 128, tru
                          {"128x128", 128, 128, true},  {"192x256", 192, 256, false},
                          {"192x128", 192, 128, false}};
 
-// 256 x 256 and 192 x 256: 2 stages (128 and 112 KiB of LDS), the next
-// stage's loads issued in the first half of the current one's
-// multiplication. 256 x 128: 3 stages, loads spread over the whole step.
-// 192 x 128 (160 KiB) and 128 x 128: 4 stages.
+// 256 x 256: 2 stages (128 KiB of LDS); 192 x 256: 3 weight stages and 2
+// activation stages (136 KiB); the next slabs' loads issued in the first
+// half of the current one's multiplication. 256 x 128: 3 stages, loads
+// spread over the whole step. 192 x 128 (160 KiB) and 128 x 128: 4 stages.
 hipError_t launch_ring(const RingCfg& c, const GemmArgs& a, int epi, const GemmSched& sc,
                        int grid, hipStream_t s) {
   // Eight waves (two per SIMD: one wave's LDS reads and barrier waits hide
@@ -834,9 +882,17 @@ hipError_t launch_ring(const RingCfg& c, const GemmArgs& a, int epi, const GemmS
   if (c.bn == 256 && c.bm == 256)
     return w4 ? dispatch_ring<256, 256, 2, 2, false>(a, epi, sc, grid, s)
               : dispatch_ring<256, 256, 2, 2, false, 8>(a, epi, sc, grid, s);
+  // 192 x 256: three weight stages and two activation stages (136 KiB),
+  // the weights requested two slabs ahead. At a 512-token prompt every CU
+  // runs one tile and each 64-k slab takes about 1.3 us, shorter than a
+  // load's latency under load: 7B gate/up 91.0 -> 82.0 us (two of each:
+  // 112 KiB; weights two ahead and activations one gave the same gain as
+  // the reverse, and three of each does not fit). At 8192 tokens the
+  // 256 x 256 tiles' longer slabs hide the latency: a third weight stage
+  // there moved nothing beyond noise.
   if (c.bn == 192 && c.bm == 256)
     return w4 ? dispatch_ring<192, 256, 2, 2, false>(a, epi, sc, grid, s)
-              : dispatch_ring<192, 256, 2, 2, false, 8>(a, epi, sc, grid, s);
+              : dispatch_ring<192, 256, 3, 2, false, 8, 2>(a, epi, sc, grid, s);
   if (c.bn == 192 && c.bm == 128)
     return w4 ? dispatch_ring<192, 128, 4, 4, false>(a, epi, sc, grid, s)
               : dispatch_ring<192, 128, 4, 4, false, 8>(a, epi, sc, grid, s);
