@@ -1,19 +1,29 @@
 """Parity at the full workload sizes, in the launch configurations the
 benchmark and the serving path use.
 
-Deep bf16 networks drift from a float32 evaluation a little more with every
-layer (about 0.25% of the hidden state per layer on these random models, the
-same as an exact bf16 evaluation on the CPU). So the oracle is applied one
-layer at a time, on the engine's own inputs to that layer, at the stated
-tolerances: a layer range cut into single-layer stages gives, bitwise, the
-same results as the uncut range (checked here too), so those stages expose
-the inputs and outputs of individual layers of the launch configuration. The
-drift across whole stacks is checked against the per-layer bf16 budget.
+Two kinds of checks against the float32 oracle:
+
+* One layer at a time, on the engine's own inputs to that layer: a layer
+  range cut into single-layer stages gives, bitwise, the same results as the
+  uncut range (checked here too), so those stages expose the inputs and
+  outputs of individual layers of the launch configuration. Per layer the
+  hidden state is within HIDDEN_TOL and the last layer + head within the
+  stated logit tolerance.
+* End to end, whole stacks from the tokens (teacher-forced on the engine's
+  tokens in decode). Over 8-40 layers a bf16-storage evaluation itself
+  drifts from the float32 definition; tests/golden/bf16_budget.json holds,
+  for exactly these sequences, how far the CPU's bf16-storage evaluation of
+  the oracle (oracle/bf16eval.py) is from the float32 oracle. The bound is
+  max(stated tolerance, MARGIN x that), so the stated 3e-2 applies wherever
+  bf16 storage can meet it.
+
 Properties that hold at any size (split == full, merged == pipeline, export
 -> import -> export, cold == warm) are checked bitwise on everything.
 """
 import concurrent.futures as cf
 import gc
+import json
+import os
 import time
 
 import numpy as np
@@ -25,13 +35,28 @@ from workloads import WORKLOADS, gen
 from tests import gpu_util as G
 
 pytestmark = [pytest.mark.gpu, pytest.mark.big]
-LOGIT_TOL = 3e-2           # one layer + head, max|err| / max|logit| (the stated tolerance)
-# One layer, relative Frobenius error of its output hidden state: an exact
-# bf16 evaluation of a single layer of these shapes is off by up to 1.2%
-# (layer 0 fed from the embedding, whose output is all new content), so the
-# bound is 2e-2; deeper layers measure 0.3-0.6%.
+LOGIT_TOL = 3e-2           # max|err| / max|logit| (the stated tolerance)
+# One layer, relative Frobenius error of its output hidden state: a
+# bf16-storage evaluation of a single layer of these shapes is off by up to
+# 1.2% (layer 0 fed from the embedding, whose output is all new content), so
+# the bound is 2e-2; deeper layers measure 0.3-0.6%.
 HIDDEN_TOL = 2e-2
-DRIFT_PER_LAYER = 3.5e-3   # bf16 drift per layer of whole stacks (measured 2.3e-3 - 2.6e-3)
+with open(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                       "bf16_budget.json")) as _f:
+    BUDGET = json.load(_f)
+
+
+def logit_bound(entry, i):
+    """Logit tolerance for check i of a budget entry (prefill = 0, then the
+    decode steps)."""
+    e = BUDGET["entries"][entry]["logit_err"]
+    return max(BUDGET["stated_logit_tol"], BUDGET["margin"] * e[min(i, len(e) - 1)])
+
+
+def hidden_bound(vals):
+    return max(1e-2, BUDGET["margin"] * max(vals))
+
+
 T0 = time.time()
 
 
@@ -138,20 +163,29 @@ def check_layer(cfg, W, layer, x_in, gpu_out, n_tok, head=False, tag=""):
 
 def test_7b_middle_stage_512_per_layer_and_cold_equals_warm():
     """Layers 8-15 of the 7B shape, one 512-token prompt (the benchmark's
-    workload): cold streaming == warm, 8 single-layer stages == the stage,
-    every layer against the oracle, KV through the export blob, decode."""
+    workload), fed the oracle's output of layers 0-7 on the prompt (bf16):
+    cold streaming == warm, 8 single-layer stages == the stage, every layer
+    against the oracle, KV through the export blob, the whole stage and two
+    decode steps against the oracle end to end."""
     torch = G.torch()
     from paper_2502_15524_amd import hs, pipeline
     wl = WORKLOADS["7b-stage8-15-cold"]
     cfg = wl.cfg
     b, e = wl.stages[wl.bench_stage]
     P = wl.prompt_lens[0]
+    say("oracle layers 0-7 on the prompt")
+    W0 = Weights(cfg, range(0, b), embed=True)
+    first = OStage(cfg, W0, 0, b)
+    x32 = gen.round_to_bf16(first.prefill([0], [P], gen.tokens(cfg.vocab, P, wl.seed)))
+    dec_in = [gen.round_to_bf16(first.decode([0], gen.tokens(cfg.vocab, 1, 100 + s)))
+              for s in range(2)]
+    del W0, first
+    gc.collect()
     say("generating weights")
     W = Weights(cfg, range(b, e))
     kw = dict(max_seqs=4, max_ctx=P + 8, max_batch_tokens=P)
     st = pipeline.Stage(cfg, b, e, **kw)
     img = pipeline.pinned_image(cfg, b, e, source=W)
-    x32 = gen.round_to_bf16(gen.hidden_input(P, cfg.hidden, wl.seed))
     x = G.to_dev_bf16(x32)
     sp = G.stream_ptr()
     outs = []
@@ -172,7 +206,6 @@ def test_7b_middle_stage_512_per_layer_and_cold_equals_warm():
     hs.hs_kv_export(st.h, [2], blob.data_ptr(), n, sp)
     torch.cuda.synchronize()
     _, kv = kvblob.parse(blob.cpu().numpy().tobytes())
-    dec_in = [gen.round_to_bf16(gen.hidden_input(1, cfg.hidden, 100 + s)) for s in range(2)]
     dec_out = []
     for s in range(2):
         od = torch.zeros((1, cfg.hidden), dtype=torch.bfloat16, device="cuda")
@@ -195,14 +228,20 @@ def test_7b_middle_stage_512_per_layer_and_cold_equals_warm():
         kg, vg = gen.bf16_bits_to_f32(kv[0][1][li]), gen.bf16_bits_to_f32(kv[0][2][li])
         assert np.abs(kg - K).max() <= 2e-2 * np.abs(K).max()
         assert np.abs(vg - V).max() <= 2e-2 * np.abs(V).max()
-    # whole stage against the oracle: within the per-layer bf16 drift budget
+    # the whole stage against the oracle from the same input
+    ent = BUDGET["entries"]["c2_7b_l8-16_p512"]
     ref = OStage(cfg, W, b, e)
     full = ref.prefill([0], [P], x32)
     drift = G.rel_fro(warm, full)
-    say(f"8-layer drift {drift:.2e} (budget {DRIFT_PER_LAYER * (e - b):.2e})")
-    assert drift <= DRIFT_PER_LAYER * (e - b)
+    bound = hidden_bound(ent["hidden_err_after_layer"][-1:])
+    say(f"8-layer stage vs oracle {drift:.2e} (bf16 evaluation "
+        f"{ent['hidden_err_after_layer'][-1]:.2e}, bound {bound:.2e})")
+    assert drift <= bound
+    dbound = hidden_bound(ent["decode_hidden_err"] + ent["hidden_err_after_layer"][-1:])
     for s in range(2):
-        assert G.rel_fro(dec_out[s], ref.decode([0], dec_in[s])) <= DRIFT_PER_LAYER * (e - b)
+        d = G.rel_fro(dec_out[s], ref.decode([0], dec_in[s]))
+        say(f"decode step {s} vs oracle {d:.2e} (bound {dbound:.2e})")
+        assert d <= dbound
     del W
     gc.collect()
 
@@ -260,6 +299,19 @@ def test_7b_full_batch8_prompt1024_decode():
         err = np.abs(d[4][0] - r31).max() / np.abs(r31).max()
         say(f"decode step {s}: layer 31 + head rel logit err {err:.2e}")
         assert err <= LOGIT_TOL
+    say("oracle end to end on sequence 0 (teacher-forced on the engine's tokens)")
+    ent = "c3_7b_full_seq0_p1024"
+    say(f"engine tokens {gtok}, oracle's greedy tokens in the budget run "
+        f"{BUDGET['entries'][ent]['oracle_tokens']}")
+    ow = OStage(cfg, W, 0, L)
+    ref = ow.prefill([0], [P], toks[:P])[-1]
+    got = [f_logits[0]] + [f_dec[s][0] for s in range(3)]
+    refs = [ref] + [ow.decode([0], np.array([gtok[s]], np.int32))[0] for s in range(3)]
+    for s, (g_, r_) in enumerate(zip(got, refs)):
+        err = np.abs(g_ - r_).max() / np.abs(r_).max()
+        say(f"32 layers + head, {'prefill' if s == 0 else f'decode step {s - 1}'}: "
+            f"rel logit err {err:.2e} (bound {logit_bound(ent, s):.2e})")
+        assert err <= logit_bound(ent, s)
     del W
     gc.collect()
 
@@ -299,6 +351,12 @@ def test_13b_two_stages_batch4_prompt2048():
     err = np.abs(out[4][i] - ref).max() / np.abs(ref).max()
     say(f"seq 1 layer 39 + head: rel logit err {err:.2e}")
     assert err <= LOGIT_TOL
+    say("oracle end to end on sequence 1 (40 layers + head)")
+    ref = OStage(cfg, W, 0, cfg.n_layers).prefill([0], [P], toks[rows])[-1]
+    err = np.abs(logits2[i] - ref).max() / np.abs(ref).max()
+    bound = logit_bound("c4_13b_full_seq1_p2048", 0)
+    say(f"seq 1, both stages: rel logit err {err:.2e} (bound {bound:.2e})")
+    assert err <= bound
     del W
     gc.collect()
 
@@ -351,10 +409,13 @@ def test_8b_gqa_four_stages_ragged_merge():
     assert merged.info()["layer_end"] == L and merged.info()["live_seqs"] == B
     mp = Pipeline.__new__(Pipeline)
     mp.cfg, mp.stages = cfg, [merged]
+    fed, merged_logits = [], []
     for s in range(3):
+        fed.append(nxt_b.cpu().numpy().copy())
         la = A.decode(ids, nxt_a)[-1]
         lm = mp.decode(ids, nxt_b)[-1]
         assert np.array_equal(la, lm) and torch.equal(nxt_a, nxt_b)
+        merged_logits.append(lm)
     A.close(), Bp.close(), mp.close()
     gc.collect()
     say("last stage cut at layer 31")
@@ -370,11 +431,26 @@ def test_8b_gqa_four_stages_ragged_merge():
         err = np.abs(c_out[4][i] - ref).max() / np.abs(ref).max()
         say(f"sequence {i} ({lens[i]} tokens): layer 31 + head rel logit err {err:.2e}")
         assert err <= LOGIT_TOL
-    # the shortest sequence end to end: within the per-layer drift budget
+    # end to end from the tokens: the shortest sequence through the pipeline
+    # and then the merged worker (teacher-forced on the engine's tokens), the
+    # longest through the pipeline
     i = int(np.argmin(lens))
-    ref = OStage(cfg, W, 0, L).prefill([0], [lens[i]], toks[starts[i]:starts[i + 1]])[-1]
-    drift = np.abs(a_out[-1][i] - ref).max() / np.abs(ref).max()
-    say(f"32-layer drift on the shortest sequence {drift:.2e}")
-    assert drift <= DRIFT_PER_LAYER * L
+    ow = OStage(cfg, W, 0, L)
+    refs = [ow.prefill([0], [lens[i]], toks[starts[i]:starts[i + 1]])[-1]]
+    refs += [ow.decode([0], np.array([fed[s][i]], np.int32))[0] for s in range(3)]
+    got = [a_out[-1][i]] + [merged_logits[s][i] for s in range(3)]
+    for s, (g_, r_) in enumerate(zip(got, refs)):
+        err = np.abs(g_ - r_).max() / np.abs(r_).max()
+        bound = logit_bound("c5_8b_full_shortest", s)
+        say(f"shortest sequence ({lens[i]} tokens), "
+            f"{'pipeline prefill' if s == 0 else f'merged decode step {s - 1}'}: "
+            f"rel logit err {err:.2e} (bound {bound:.2e})")
+        assert err <= bound
+    j = int(np.argmax(lens))
+    ref = OStage(cfg, W, 0, L).prefill([0], [lens[j]], toks[starts[j]:starts[j + 1]])[-1]
+    err = np.abs(a_out[-1][j] - ref).max() / np.abs(ref).max()
+    bound = logit_bound("c5_8b_full_longest", 0)
+    say(f"longest sequence ({lens[j]} tokens): rel logit err {err:.2e} (bound {bound:.2e})")
+    assert err <= bound
     del W
     gc.collect()
