@@ -946,7 +946,7 @@ def bench_kernel_name(rocprof_name):
     """The launch name bench.py reports (LaunchInfo) for a rocprofv3 kernel
     name, and the source file of the kernel; (None, None) for others."""
     import re
-    m = re.search(r"gemm_ring<(\d+), (\d+), \d+, \d+, (true|false), (\d+)>", rocprof_name)
+    m = re.search(r"gemm_ring<(\d+), (\d+), \d+, \d+, (true|false), (\d+)[,>]", rocprof_name)
     if m:
         sk = "sk" if m.group(3) == "true" else ""
         return f"gemm_r{m.group(1)}x{m.group(2)}{sk}_{_EPI_NAMES[int(m.group(4))]}", "k_gemm"

@@ -110,7 +110,12 @@ def test_gemm_split_k_shapes(N, K, epi):
 @pytest.mark.parametrize("lens,nh,nkv,d", [
     ([1], 4, 4, 64), ([5, 64, 65], 4, 2, 64), ([130, 7, 300], 4, 4, 128),
     ([257], 8, 2, 128), ([64, 128, 1, 33], 2, 1, 128),
-    ([1024, 1024], 32, 8, 128)])     # enough 128-query tiles for the 8-wave variant
+    ([1024, 1024], 32, 8, 128),      # enough 128-query tiles for the 8-wave variant
+    # 4-wave tiles that do not fit one workgroup per CU (no key split):
+    # workgroup counts 512 and 380 (D = 128), 320 and 276 (D = 64), so both
+    # multiples of 8 and others
+    ([1024], 32, 8, 128), ([1000, 150], 20, 5, 128), ([900, 300], 16, 4, 64),
+    ([1000, 400], 12, 6, 64)])
 def test_attn_prefill(lens, nh, nkv, d):
     torch = G.torch()
     hs = _hs()
