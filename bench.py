@@ -276,7 +276,7 @@ def bench_c2(args):
     img = pipeline.pinned_image(cfg, b, e)
     log(f"[bench] packed stage image {img.numel() / 1e9:.3f} GB in {time.perf_counter() - t:.1f} s")
     out = torch.empty((P, H), dtype=torch.bfloat16, device=dev)
-    max_ctx = P + args.decode_steps + 16
+    max_ctx = P + max(args.decode_steps, 9) + 16
     st = pipeline.Stage(cfg, b, e, max_seqs=4, max_ctx=max_ctx, max_batch_tokens=P,
                         n_copy_streams=args.copy_streams)
     chunk = args.chunk_mb << 20
@@ -440,7 +440,7 @@ def bench_c2(args):
     for _ in range(4):
         dec()
     stream.synchronize()
-    nd = args.decode_steps - 8
+    nd = max(args.decode_steps - 8, 1)
     ev0.record(stream)
     for _ in range(nd):
         dec()

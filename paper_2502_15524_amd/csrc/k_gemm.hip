@@ -342,7 +342,9 @@ void gemm_ring(GemmArgs a, GemmSched sc) {
   // loads only make the vmcnt waits of the ring stricter: loads complete in
   // order.)
   constexpr bool ROPE_PRE = EPI == EPI_QKV_ROPE && !SK;
-  constexpr bool ROPE_TAB = ROPE_PRE && TN * TM <= 32;
+  // (the cos/sin rows take 4 TN TM registers: with eight waves, two per
+  // SIMD, only the small tiles have room; 256 x 256 spilled 100 registers)
+  constexpr bool ROPE_TAB = ROPE_PRE && TN * TM <= (NW == 4 ? 32 : 16);
   constexpr int RJ = ROPE_PRE ? TM : 1, RJT = ROPE_TAB ? TM : 1, RI = ROPE_TAB ? TN / 2 : 1;
   int r_pos[RJ], r_slot[RJ];
   float4 r_cos[RJT][RI], r_sin[RJT][RI];
@@ -897,11 +899,11 @@ hipError_t launch_ring(const RingCfg& c, const GemmArgs& a, int epi, const GemmS
     return w4 ? dispatch_ring<192, 128, 4, 4, false>(a, epi, sc, grid, s)
               : dispatch_ring<192, 128, 4, 4, false, 8>(a, epi, sc, grid, s);
   if (c.bn == 256 && c.bm == 128) {
-    if (w4)
-      return sc.sk ? dispatch_ring<256, 128, 3, 4, true>(a, epi, sc, grid, s)
-                   : dispatch_ring<256, 128, 3, 4, false>(a, epi, sc, grid, s);
-    return sc.sk ? dispatch_ring<256, 128, 3, 4, true, 8>(a, epi, sc, grid, s)
-                 : dispatch_ring<256, 128, 3, 4, false, 8>(a, epi, sc, grid, s);
+    // stream-K 256 x 128 keeps four waves (its partial-tile reduction does
+    // not fit the registers of eight: 125-138 spilled)
+    if (sc.sk) return dispatch_ring<256, 128, 3, 4, true>(a, epi, sc, grid, s);
+    return w4 ? dispatch_ring<256, 128, 3, 4, false>(a, epi, sc, grid, s)
+              : dispatch_ring<256, 128, 3, 4, false, 8>(a, epi, sc, grid, s);
   }
   if (w4)
     return sc.sk ? dispatch_ring<128, 128, 4, 4, true>(a, epi, sc, grid, s)
