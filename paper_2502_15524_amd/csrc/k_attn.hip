@@ -602,17 +602,22 @@ __global__ __launch_bounds__(256) void attn_decode_split_kernel(AttnDecodeArgs a
 }
 
 // MFMA form of the split kernel for grouped-query heads (G >= 2, D = 128).
-// Wave w takes tokens 32w .. 32w + 31 of the split (two cache blocks).
+// Wave w takes tokens 32w .. 32w + 31 of the split (two cache blocks). The
+// keys and values are read with whole-row loads (each instruction covers 4
+// rows of 256 bytes, lane l taking chunk l % 16 of row l / 16; the MFMA
+// operand order, 64 bytes of each of 16 rows per instruction, streamed
+// 15-17% slower on MI355X) and staged row-major through the wave's LDS
+// buffer: first the keys, read back in operand order, then the values.
 // Scores are formed transposed, S^T = K Q^T, with 16x16x32 MFMAs: the keys
-// on the rows (lane (r, g) loads key r of a block, d-chunk g of each 32-d
-// step, straight from the pool) and the G query heads of the kv head on the
-// columns (the other columns zero), so lane (r, g) ends with the scores of
-// keys 4g .. 4g+3 (and 16 + 4g .. 16 + 4g + 3) for query head r. The values
-// are staged row-major in the wave's LDS buffer and P V^T reads its V^T
-// fragments with transposing LDS reads (as the prefill kernel does); the
+// on the rows (lane (r, g) holds key r of a block, d-chunk g of each 32-d
+// step) and the G query heads of the kv head on the columns (the other
+// columns zero), so lane (r, g) ends with the scores of keys 4g .. 4g+3 (and
+// 16 + 4g .. 16 + 4g + 3) for query head r. P V^T reads its V^T fragments
+// with transposing LDS reads (as the prefill kernel does); the
 // probabilities are the B operand exactly as the score MFMAs left them.
 // With fused RoPE the rotation pairs (d, d + D/2) sit in one lane. The
-// waves' partial results are merged through LDS in wave order.
+// waves' partial results are merged through LDS in wave order; each wave's
+// partial reuses its own (by then consumed) value buffer.
 typedef short s16x4_dv __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ void rope_pair(pack8& x1, pack8& x2, const float* cs, const float* sn) {
@@ -627,7 +632,8 @@ __device__ __forceinline__ void rope_pair(pack8& x1, pack8& x2, const float* cs,
 }
 
 template <int G, bool ROPE>
-__global__ __launch_bounds__(256) void attn_decode_gqa_kernel(AttnDecodeArgs a, float scale_log2) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void attn_decode_gqa_kernel(
+    AttnDecodeArgs a, float scale_log2) {
   constexpr int D = 128;
   static_assert(G >= 2 && G <= 16, "the query heads of a kv head fit the 16 MFMA columns");
   static_assert(kDecodeSplit == 128, "four waves of two cache blocks");
@@ -637,7 +643,10 @@ __global__ __launch_bounds__(256) void attn_decode_gqa_kernel(AttnDecodeArgs a, 
   constexpr int BPS = kDecodeSplit / 16;
   __shared__ __attribute__((aligned(16))) bf16_t sV[4][32 * LV];
   __shared__ float s_ml[4][G][2];
-  __shared__ __attribute__((aligned(16))) float s_acc[4][G][D];
+  // wave w's partial output [G][D] reuses its own value buffer (read by
+  // that wave only, and consumed before the partial is written)
+  static_assert(G * D * 4 <= 32 * LV * 2, "a wave's partial fits its value buffer");
+  const auto s_acc = [&](int w) { return reinterpret_cast<float*>(sV[w]); };
 
   const int split = blockIdx.x, kh = blockIdx.y, b = blockIdx.z;
   const int32_t* bt = a.block_table + (int64_t)b * a.max_blocks;
@@ -656,9 +665,13 @@ __global__ __launch_bounds__(256) void attn_decode_gqa_kernel(AttnDecodeArgs a, 
   const bf16_t* qrow = a.q + (int64_t)b * a.ldq;
   const int tb = t_begin + wave * 32;  // first token of this wave
 
-  pack8 kf[2][KS], vf[2][KS], qf[KS];
-  bool live[2], is_new[2];
+  pack8 kf[2][KS], ck[2][4], cv[2][4], qf[KS];
+  bool is_new[2];
   int ph[2];
+  // whole-row loads: instruction i of block t takes rows 4i .. 4i + 3 of the
+  // block (lane l: row 4i + l / 16, 16-byte chunk l % 16); all of them go
+  // out first (non-temporal: each cached byte is read once per step)
+  const int crow = lane >> 4, cch = lane & 15;
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
     const int blk = wave * 2 + t;
@@ -666,22 +679,50 @@ __global__ __launch_bounds__(256) void attn_decode_gqa_kernel(AttnDecodeArgs a, 
 #pragma unroll
     for (int j = 1; j < BPS; ++j) p = blk == j ? phys[j] : p;
     ph[t] = p;
-    const int tok = tb + 16 * t + fr;
-    live[t] = tok < ctx;
-    is_new[t] = ROPE && tok == ctx - 1;
-    const bf16_t* krow = a.pool + ((int64_t)p * 2 * a.n_kv_heads + kh) * 16 * D + fr * D;
-    const bf16_t* vrow = krow + kv_stride;
-    if (is_new[t]) {  // not in the pool yet: the projection's rows
-      krow = qrow + (int64_t)(a.n_heads + kh) * D;
-      vrow = qrow + (int64_t)(a.n_heads + a.n_kv_heads + kh) * D;
-    }
-    // all key and value loads go out first (non-temporal: each cached byte
-    // is read once per step)
+    is_new[t] = ROPE && tb + 16 * t + fr == ctx - 1;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      kf[t][ks] = live[t] ? ld16_nt(krow + ks * 32 + g * 8) : zero8();
-      vf[t][ks] = live[t] ? ld16_nt(vrow + ks * 32 + g * 8) : zero8();
+    for (int i = 0; i < 4; ++i) {
+      const int r = 4 * i + crow, tok = tb + 16 * t + r;
+      const bf16_t* krow = a.pool + ((int64_t)p * 2 * a.n_kv_heads + kh) * 16 * D + r * D;
+      const bf16_t* vrow = krow + kv_stride;
+      if (ROPE && tok == ctx - 1) {  // not in the pool yet: the projection's rows
+        krow = qrow + (int64_t)(a.n_heads + kh) * D;
+        vrow = qrow + (int64_t)(a.n_heads + a.n_kv_heads + kh) * D;
+      }
+      ck[t][i] = tok < ctx ? ld16_nt(krow + cch * 8) : zero8();
+      cv[t][i] = tok < ctx ? ld16_nt(vrow + cch * 8) : zero8();
     }
+  }
+  // keys row-major into this wave's buffer (key 16 t + row), read back in
+  // the score MFMAs' operand order; then the values over them (one wave's
+  // LDS operations run in order)
+  bf16_t* sv = sV[wave];
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      *reinterpret_cast<pack8*>(sv + (16 * t + 4 * i + crow) * LV + cch * 8) = ck[t][i];
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      kf[t][ks] = *reinterpret_cast<const pack8*>(sv + (16 * t + fr) * LV + ks * 32 + g * 8);
+  asm volatile("" ::: "memory");  // the key reads before the value stores
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      *reinterpret_cast<pack8*>(sv + (16 * t + 4 * i + crow) * LV + cch * 8) = cv[t][i];
+  if constexpr (ROPE) {  // the new token's value into its pool slot (its key below, rotated)
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = 4 * i + crow;
+        if (tb + 16 * t + r == ctx - 1)
+          st16(a.pool_w + ((int64_t)ph[t] * 2 * a.n_kv_heads + kh) * 16 * D + kv_stride + r * D + cch * 8,
+               cv[t][i]);
+      }
   }
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks)
@@ -696,16 +737,16 @@ __global__ __launch_bounds__(256) void attn_decode_gqa_kernel(AttnDecodeArgs a, 
       float cs[8], sn[8];
 #pragma unroll
       for (int e = 0; e < 8; e += 4) {
-        const float4 cv = *reinterpret_cast<const float4*>(ct + ks * 32 + g * 8 + e);
-        const float4 sv = *reinterpret_cast<const float4*>(st + ks * 32 + g * 8 + e);
-        cs[e] = cv.x;
-        cs[e + 1] = cv.y;
-        cs[e + 2] = cv.z;
-        cs[e + 3] = cv.w;
-        sn[e] = sv.x;
-        sn[e + 1] = sv.y;
-        sn[e + 2] = sv.z;
-        sn[e + 3] = sv.w;
+        const float4 c4 = *reinterpret_cast<const float4*>(ct + ks * 32 + g * 8 + e);
+        const float4 s4 = *reinterpret_cast<const float4*>(st + ks * 32 + g * 8 + e);
+        cs[e] = c4.x;
+        cs[e + 1] = c4.y;
+        cs[e + 2] = c4.z;
+        cs[e + 3] = c4.w;
+        sn[e] = s4.x;
+        sn[e + 1] = s4.y;
+        sn[e + 2] = s4.z;
+        sn[e + 3] = s4.w;
       }
       rope_pair(qf[ks], qf[ks + KS / 2], cs, sn);
 #pragma unroll
@@ -714,22 +755,12 @@ __global__ __launch_bounds__(256) void attn_decode_gqa_kernel(AttnDecodeArgs a, 
     }
 #pragma unroll
     for (int t = 0; t < 2; ++t)
-      if (is_new[t]) {  // append the rotated key and the value to the cache
+      if (is_new[t]) {  // append the rotated key to the cache
         bf16_t* kd = a.pool_w + ((int64_t)ph[t] * 2 * a.n_kv_heads + kh) * 16 * D + fr * D;
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          st16(kd + ks * 32 + g * 8, kf[t][ks]);
-          st16(kd + kv_stride + ks * 32 + g * 8, vf[t][ks]);
-        }
+        for (int ks = 0; ks < KS; ++ks) st16(kd + ks * 32 + g * 8, kf[t][ks]);
       }
   }
-
-  // values row-major into this wave's buffer (key 16 t + r, chunk 4 ks + g)
-  bf16_t* sv = sV[wave];
-#pragma unroll
-  for (int t = 0; t < 2; ++t)
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) st16(sv + (16 * t + fr) * LV + ks * 32 + g * 8, vf[t][ks]);
 
   // S^T: lane (r, g) gets keys tb + 16 t + 4g + j of query head r
   f32x4_v s[2];
@@ -785,7 +816,7 @@ __global__ __launch_bounds__(256) void attn_decode_gqa_kernel(AttnDecodeArgs a, 
   if (fr < G) {
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
-      *reinterpret_cast<f32x4_v*>(&s_acc[wave][fr][dt * 16 + 4 * g]) = o[dt];
+      *reinterpret_cast<f32x4_v*>(s_acc(wave) + fr * D + dt * 16 + 4 * g) = o[dt];
     if (g == 0) {
       s_ml[wave][fr][0] = ms;
       s_ml[wave][fr][1] = l;
@@ -806,7 +837,7 @@ __global__ __launch_bounds__(256) void attn_decode_gqa_kernel(AttnDecodeArgs a, 
       if (mw == -INFINITY) continue;
       const float f = fast_exp2(mw - M);
       L += s_ml[w][gg][1] * f;
-      O += s_acc[w][gg][d] * f;
+      O += s_acc(w)[gg * D + d] * f;
     }
     const int64_t row = base + gg * a.max_splits + split;
     a.part_o[row * D + d] = O;
