@@ -622,6 +622,17 @@ void gemm_ring(GemmArgs a, GemmSched sc) {
 // straight from global memory makes every instruction touch half of each of
 // 16 rows; the whole-block loads stream 10-30% faster on MI355X.) The loads
 // of the next slab group are issued before the current one is multiplied.
+//
+// The activations (the B operand, tokens on the MFMA columns) are loaded in
+// fragment order, lane (fr, g) taking chunk 4 ks + g of token fr: 64 bytes of
+// each of 16 rows per instruction. With XS they take the weights' route
+// instead: instruction h of a 16-token chunk reads whole 128-byte rows of
+// tokens 8h .. 8h + 7 (lane L: token 8h + L/8, chunk (L % 8) ^ (L / 8)) and
+// stores them to position 64 h + L of the wave's activation buffer, which
+// then has the layout of a weight tile's image and is read like one. The
+// MFMA operands are the same either way; staging pays off once many tokens
+// share the call (8B-shape o and down projections at 16 tokens, MI355X:
+// 12.3 -> 9.7 and 26.5 -> 23.5 us) and costs about 0.5 us at one token.
 
 // With NORM, X is the un-normalised residual stream and the GEMM applies the
 // RMSNorm of its rows itself: each loaded activation chunk is multiplied by
@@ -629,9 +640,12 @@ void gemm_ring(GemmArgs a, GemmSched sc) {
 // of the raw values are summed along the way, and the epilogue scales each
 // token's outputs by 1 / sqrt(mean square + eps). Used for decode, where the
 // separate norm kernel would cost a launch per projection.
-template <int NF, int MCH, int U, int EPI, bool NORM, int WV>
+template <int NF, int MCH, int U, int EPI, bool NORM, int WV, bool XS>
 __global__ __launch_bounds__(64 * WV) void gemm_skinny(GemmArgs a) {
   static_assert(EPI != EPI_SWIGLU || (NF % 2) == 0, "SwiGLU needs gate/up tile pairs");
+  // the norm's sums of squares follow the fragment-order loads; keeping one
+  // order for every batch size keeps a token's result independent of M
+  static_assert(!(NORM && XS), "staged activations are built without the fused norm");
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n0 = blockIdx.x * 16 * NF;
   const int kp = (a.K + 63) & ~63;
@@ -649,13 +663,20 @@ __global__ __launch_bounds__(64 * WV) void gemm_skinny(GemmArgs a) {
   const int r8 = fr % 8;
   // 16-byte position of lane (fr, g)'s row inside the 2 KiB image of a 16-row tile
   const int fpos = (fr / 8) * 64 + r8 * 8;
-  const bf16_t* xrow[MCH];
+  // activation rows: XS, load i = 2 c + h (instruction h of token chunk c):
+  // token 8 i + L / 8 from chunk (L % 8) ^ (L / 8) on; otherwise load c: token
+  // 16 c + fr (the chunk offset added per load)
+  constexpr int XH = XS ? 2 : 1;
+  const int xr = lane >> 3, xc = (lane & 7) ^ (lane >> 3);
+  const bf16_t* xrow[MCH * XH];
 #pragma unroll
-  for (int c = 0; c < MCH; ++c) {
-    const int m = 16 * c + fr;
-    xrow[c] = (m < a.M) ? a.X + (int64_t)m * a.ldx : nullptr;
+  for (int i = 0; i < MCH * XH; ++i) {
+    const int m = XS ? 8 * i + xr : 16 * i + fr;
+    xrow[i] = (m < a.M) ? a.X + (int64_t)m * a.ldx + (XS ? xc * 8 : 0) : nullptr;
   }
-  __shared__ pack8 wlds[WV][U][NF * 128];
+  // per wave and slab: the weight tiles' images, then with XS the activation
+  // chunks' images (16-byte units)
+  __shared__ pack8 wlds[WV][U][(NF + (XS ? MCH : 0)) * 128];
 
   f32x4_v acc[NF][MCH];
   float ssq[MCH];
@@ -691,6 +712,7 @@ __global__ __launch_bounds__(64 * WV) void gemm_skinny(GemmArgs a) {
 #pragma unroll
         for (int h = 0; h < 2; ++h) wlds[wave][u][(2 * f + h) * 64 + lane] = wv[u][f][h];
     if (s0 + U < se) load_w(s0 + U);
+    // activations: XS, whole rows (stored below); else fragment order, xv[c][u][ks]
     pack8 xv[MCH][U][2], gv[U][2];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -700,8 +722,12 @@ __global__ __launch_bounds__(64 * WV) void gemm_skinny(GemmArgs a) {
       for (int ks = 0; ks < 2; ++ks) {
         const int chunk = ks * 4 + g;
 #pragma unroll
-        for (int c = 0; c < MCH; ++c)
-          xv[c][u][ks] = (ok && xrow[c]) ? ld16(xrow[c] + sl * 64 + chunk * 8) : zero8();
+        for (int c = 0; c < MCH; ++c) {
+          if constexpr (XS)
+            xv[c][u][ks] = (ok && xrow[2 * c + ks]) ? ld16(xrow[2 * c + ks] + sl * 64) : zero8();
+          else
+            xv[c][u][ks] = (ok && xrow[c]) ? ld16(xrow[c] + sl * 64 + chunk * 8) : zero8();
+        }
         if constexpr (NORM) gv[u][ks] = ok ? ld16(a.norm_gain + sl * 64 + chunk * 8) : zero8();
       }
     }
@@ -721,11 +747,24 @@ __global__ __launch_bounds__(64 * WV) void gemm_skinny(GemmArgs a) {
             }
           }
     }
+    if constexpr (XS) {
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int c = 0; c < MCH; ++c)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) wlds[wave][u][NF * 128 + (2 * c + h) * 64 + lane] = xv[c][u][h];
+    }
     asm volatile("" ::: "memory");  // keep the fragment reads after the stores
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
+      for (int ks = 0; ks < 2; ++ks) {
+        if constexpr (XS) {  // the fragments from the staged image (read like a weight tile's)
+#pragma unroll
+          for (int c = 0; c < MCH; ++c)
+            xv[c][u][ks] = wlds[wave][u][(NF + c) * 128 + fpos + ((ks * 4 + g) ^ r8)];
+        }
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
           const pack8 w = wlds[wave][u][f * 128 + fpos + ((ks * 4 + g) ^ r8)];
@@ -734,6 +773,7 @@ __global__ __launch_bounds__(64 * WV) void gemm_skinny(GemmArgs a) {
             acc[f][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                 as_bf16x8(w), as_bf16x8(xv[c][u][ks]), acc[f][c], 0, 0, 0);
         }
+      }
     asm volatile("" ::: "memory");  // and the next stores after these reads
   }
 
@@ -793,52 +833,54 @@ __global__ __launch_bounds__(64 * WV) void gemm_skinny(GemmArgs a) {
 
 namespace {
 
-template <int NF, int MCH, int U, int WV, bool NORM>
+template <int NF, int MCH, int U, int WV, bool XS, bool NORM>
 hipError_t dispatch_skinny_norm(const GemmArgs& a, int epi, hipStream_t s) {
   const int grid = (a.N + 16 * NF - 1) / (16 * NF);
   const dim3 blk(64 * WV);
   switch (epi) {
     case EPI_STORE:
-      hipLaunchKernelGGL((gemm_skinny<NF, MCH, U, EPI_STORE, NORM, WV>), dim3(grid), blk, 0, s, a);
+      hipLaunchKernelGGL((gemm_skinny<NF, MCH, U, EPI_STORE, NORM, WV, XS>), dim3(grid), blk, 0, s, a);
       break;
     case EPI_RESID:
-      hipLaunchKernelGGL((gemm_skinny<NF, MCH, U, EPI_RESID, NORM, WV>), dim3(grid), blk, 0, s, a);
+      hipLaunchKernelGGL((gemm_skinny<NF, MCH, U, EPI_RESID, NORM, WV, XS>), dim3(grid), blk, 0, s, a);
       break;
     case EPI_SWIGLU:
       if constexpr (NF % 2 == 0) {
-        hipLaunchKernelGGL((gemm_skinny<NF, MCH, U, EPI_SWIGLU, NORM, WV>), dim3(grid), blk, 0, s, a);
+        hipLaunchKernelGGL((gemm_skinny<NF, MCH, U, EPI_SWIGLU, NORM, WV, XS>), dim3(grid), blk, 0, s, a);
         break;
       } else {
         return hipErrorInvalidValue;
       }
     case EPI_F32:
-      hipLaunchKernelGGL((gemm_skinny<NF, MCH, U, EPI_F32, NORM, WV>), dim3(grid), blk, 0, s, a);
+      hipLaunchKernelGGL((gemm_skinny<NF, MCH, U, EPI_F32, NORM, WV, XS>), dim3(grid), blk, 0, s, a);
       break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-template <int NF, int MCH, int U, int WV>
+template <int NF, int MCH, int U, int WV, bool XS = false>
 hipError_t dispatch_epi_skinny(const GemmArgs& a, int epi, hipStream_t s) {
   if (a.norm_gain) {
     // the fused norm is only built for one 16-token chunk (decode batches)
-    if constexpr (MCH == 1) return dispatch_skinny_norm<NF, 1, U, WV, true>(a, epi, s);
+    if constexpr (MCH == 1 && !XS) return dispatch_skinny_norm<NF, 1, U, WV, false, true>(a, epi, s);
     else return hipErrorInvalidValue;
   }
-  return dispatch_skinny_norm<NF, MCH, U, WV, false>(a, epi, s);
+  return dispatch_skinny_norm<NF, MCH, U, WV, XS, false>(a, epi, s);
 }
 
 // The skinny variants built for one 16-token chunk, as (rows per workgroup /
-// 16, slabs unrolled per wave, waves per workgroup): the ones the selection
-// in gemm() takes.
-#define HS_SKINNY_MCH1(X) \
-  X(1, 1, 8) X(1, 2, 8) X(2, 1, 8) X(2, 1, 4) X(4, 1, 4) X(2, 1, 2) X(4, 1, 2) X(8, 1, 2) X(1, 1, 16) \
-  X(3, 1, 16)
+// 16, slabs unrolled per wave, waves per workgroup, staged activations): the
+// ones the selection in gemm() takes.
+#define HS_SKINNY_MCH1(X)                                                                      \
+  X(1, 1, 8, false) X(2, 1, 8, false) X(2, 1, 4, false) X(4, 1, 4, false) X(2, 1, 2, false) \
+  X(4, 1, 2, false) X(8, 1, 2, false) X(1, 1, 16, false) X(3, 1, 16, false) X(1, 1, 16, true)
 
-hipError_t dispatch_skinny1(const GemmArgs& a, int epi, int nf, int u, int wv, hipStream_t s) {
-#define HS_SKINNY_CASE(NF_, U_, WV_) \
-  if (nf == NF_ && u == U_ && wv == WV_) return dispatch_epi_skinny<NF_, 1, U_, WV_>(a, epi, s);
+hipError_t dispatch_skinny1(const GemmArgs& a, int epi, int nf, int u, int wv, bool xs,
+                            hipStream_t s) {
+#define HS_SKINNY_CASE(NF_, U_, WV_, XS_)                  \
+  if (nf == NF_ && u == U_ && wv == WV_ && xs == XS_) \
+    return dispatch_epi_skinny<NF_, 1, U_, WV_, XS_>(a, epi, s);
   HS_SKINNY_MCH1(HS_SKINNY_CASE)
 #undef HS_SKINNY_CASE
   return hipErrorInvalidValue;
@@ -970,23 +1012,26 @@ hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info) {
     // by the rotation pass
     const int pe = epi == EPI_QKV_ROPE ? EPI_STORE : epi;
     const int mch = (a.M + 15) / 16;
-    // Rows per workgroup (16 NF), 64-k slabs per load group (U) and waves per
-    // workgroup (WV) for one token chunk, from a sweep on MI355X over the
-    // decode projections of 7B, 8B and 13B models at 1, 4, 8 and 16 tokens:
-    // narrow outputs (o, down, QKV up to 8192 wide) fill the chip with eight
-    // waves per workgroup (sixteen for a 4096 x 4096 o projection), wide QKV
-    // and gate/up with four; gate/up takes four
-    // row tiles per workgroup once that still gives 1.5 workgroups per CU
-    // (8B, 13B: 38 and 45 instead of 43 and 52 us); o/down wider than one
-    // row tile per CU take one slab per group up to 4 tokens and two row
-    // tiles above; the LM head runs two waves over as many row tiles as keep
-    // about a thousand workgroups (128256 wide: 155 instead of 162-169 us).
-    // WV depends on the shape only, never on M, so that a token's result (its
-    // k order) does not depend on how many tokens share the call.
-    // HS_SKINNY_CFG="<NF>,<U>,<WV>" forces a choice (tuning only).
-    static const char* force = getenv("HS_SKINNY_CFG");
+    // Rows per workgroup (16 NF), 64-k slabs per load group (U), waves per
+    // workgroup (WV) and staged activations (XS) for one token chunk, from
+    // sweeps on MI355X over the decode projections of 7B, 8B and 13B models
+    // at 1, 4, 8 and 16 tokens: o and down projections up to one row tile
+    // per CU run sixteen waves of one row tile (7B down at 1 and 8 tokens:
+    // 17.4 -> 16.2 and 18.2 -> 16.9 us against eight waves and two slabs per
+    // group), with the activations staged from 8 tokens on; wider ones eight
+    // waves, two row tiles above 4 tokens. QKV up to 8192 wide takes eight
+    // waves, wide QKV and gate/up four; gate/up takes four row tiles per
+    // workgroup once that still gives 1.5 workgroups per CU (8B, 13B: 38 and
+    // 45 instead of 43 and 52 us); the LM head runs two waves over as many
+    // row tiles as keep about a thousand workgroups (128256 wide: 155 instead
+    // of 162-169 us). WV depends on the shape only, never on M, so that a
+    // token's result (its k order) does not depend on how many tokens share
+    // the call; XS changes only how the same operands reach the MFMAs.
+    // HS_SKINNY_CFG="<NF>,<U>,<WV>[,<XS>]" forces a choice (tuning only; read
+    // on every call so that a sweep can change it between calls).
+    const char* force = getenv("HS_SKINNY_CFG");
     const int cus = device_cus();
-    int nf = 1, u = 1, wv = 4;
+    int nf = 1, u = 1, wv = 4, xs = 0;
     if (pe == EPI_F32) {
       nf = 2, wv = 2;
       while (nf < 8 && a.N / (16 * nf) > 1100) nf *= 2;
@@ -994,19 +1039,22 @@ hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info) {
       nf = (a.N / 64 >= cus + cus / 2) ? 4 : 2;
     } else if (pe == EPI_RESID) {
       wv = 8;
-      if (a.N / 16 > cus) nf = a.M > 4 ? 2 : 1;
-      else if (a.K <= 4096) wv = 16;  // 4096 x 4096 o projection: 9.4 -> 8.2 us at 8 tokens
-      else u = a.M <= 8 ? 2 : 1;
+      if (a.N / 16 > cus) {
+        nf = a.M > 4 ? 2 : 1;
+      } else {
+        wv = 16;
+        xs = a.M >= 8;
+      }
     } else if (pe == EPI_STORE) {
       nf = 2, wv = a.N <= 8192 ? 8 : 4;
       // three row tiles when that gives one workgroup per CU (7B QKV: 256 x
       // 48 rows; 21.5 -> 19.5 us)
       if (a.N % 48 == 0 && a.N / 48 <= cus && a.N / 48 > cus * 3 / 4) nf = 3, wv = 16;
     }
-    if (force && *force) sscanf(force, "%d,%d,%d", &nf, &u, &wv);
+    if (force && *force) sscanf(force, "%d,%d,%d,%d", &nf, &u, &wv, &xs);
     if (pe == EPI_SWIGLU && (nf % 2)) nf = 2;
     if (mch == 1) {
-      e = dispatch_skinny1(a, pe, nf, u, wv, s);
+      e = dispatch_skinny1(a, pe, nf, u, wv, xs != 0, s);
     } else if (pe == EPI_SWIGLU) {
       switch (mch) {
         case 2: e = dispatch_epi_skinny<2, 2, 2, 4>(a, pe, s); break;
