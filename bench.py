@@ -950,7 +950,7 @@ def bench_kernel_name(rocprof_name):
     if m:
         sk = "sk" if m.group(3) == "true" else ""
         return f"gemm_r{m.group(1)}x{m.group(2)}{sk}_{_EPI_NAMES[int(m.group(4))]}", "k_gemm"
-    m = re.search(r"gemm_skinny<\d+, \d+, \d+, (\d+), (true|false), \d+>", rocprof_name)
+    m = re.search(r"gemm_skinny<\d+, \d+, \d+, (\d+), (true|false), \d+[,>]", rocprof_name)
     if m:
         norm = "norm_" if m.group(2) == "true" else ""
         return f"gemm_skinny_{norm}{_EPI_NAMES[int(m.group(1))]}", "k_gemm"
@@ -1014,8 +1014,8 @@ def summarize_counters(fetch_csv, write_csv, workload):
             # the probe's copies are one export of every stage and one import
             # of all blobs: two operations of equal size
             hbm = (f * sf + w * sw) * 1024 / 2
-        elif len(owners[bname]) > 1:
-            continue      # two launch sites share the name (o and down): no line
+        elif len(owners[bname]) > 1 or bname.endswith("_resid"):
+            continue      # the o and down launch sites share the name: no line
         lines.append(f"traffic: kernel={bname} workload={workload} hbm_bytes_per_launch="
                      f"{int(hbm)} {src}_sha256={_sha(os.path.join(csrc, src + '.hip'))}")
     if attn:

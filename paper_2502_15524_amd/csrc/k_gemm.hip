@@ -1081,7 +1081,8 @@ hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info) {
     // takes (flops / CUs) / its rate plus a fixed cost for the pipeline
     // start-ups and the partial-tile reductions. The rates are per-CU
     // TFLOP/s measured on MI355X with weights streamed from HBM.
-    // HS_GEMM_CFG="<tile>[,dp|,sk][,g<n>]" forces a choice (tuning only).
+    // HS_GEMM_CFG="<tile>[,dp|,sk][,g<n>]" forces a choice (tuning only; read
+    // on every call so that a sweep can change it between calls).
     const int cus = device_cus();
     const int nk = (int)(kp / 64);
     struct Cand { const RingCfg* c; bool sk; double rate; };
@@ -1125,7 +1126,7 @@ hipError_t gemm(const GemmArgs& a, int epi, hipStream_t s, LaunchInfo* info) {
       }
     }
     int group = 8;
-    static const char* force = getenv("HS_GEMM_CFG");
+    const char* force = getenv("HS_GEMM_CFG");  // read per call (tuning sweeps)
     if (force && *force) {
       std::string f(force);
       for (const RingCfg& c : kRing)  // longest matching name wins
