@@ -220,6 +220,11 @@ __device__ __forceinline__ void ring_stage(f32x4_v (&acc)[TN][TM], bf16x8_v (&a)
   using T = RTile<BN, BM, BK, NS, NW>;
   constexpr int CPR = T::CPR, KS = BK / 32;
   constexpr int MASK_MFMA = 0x008, MASK_DS_READ = 0x100;
+  // 256 x 256 tiles: a wave runs its MFMA groups at raised priority, so the
+  // SIMD's other wave issues its LDS reads and loads in between instead of
+  // competing with them (8192 tokens, MI355X: gate/up 1155-1162 -> 1107-1113
+  // us, down 580 -> 562; the smaller tiles gained nothing)
+  constexpr bool PRIO = BN == 256 && BM == 256 && NW == 8;
   static_assert(TN % 2 == 0 && KS == 2, "the deferred row tile uses a[1] and b[1]");
 #pragma unroll
   for (int j = 0; j < TM; ++j) b[0][j] = lds_frag<CPR>(sx, wm * T::WM + j * 16 + fr, g);
@@ -249,9 +254,11 @@ __device__ __forceinline__ void ring_stage(f32x4_v (&acc)[TN][TM], bf16x8_v (&a)
         a[nxt] = lds_frag<CPR>(sw, wn * T::WN + fr, c + 4);
       }
       if (ks + 1 == KS && i + 1 == TN) break;  // deferred to the next stage (or the end)
+      if constexpr (PRIO) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int j = 0; j < TM; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[cur], b[ks & 1][j], acc[i][j], 0, 0, 0);
+      if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
       if (i + 1 < TN) __builtin_amdgcn_sched_group_barrier(MASK_DS_READ, 1, 0);
       else if (ks + 1 < KS) __builtin_amdgcn_sched_group_barrier(MASK_DS_READ, TM + 1, 0);
       __builtin_amdgcn_sched_group_barrier(MASK_MFMA, TM, 0);
