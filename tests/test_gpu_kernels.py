@@ -70,6 +70,40 @@ def test_gemm(M, N, K, epi):
     assert err <= tol, (err, scale)
 
 
+@pytest.mark.parametrize("M,N,K", [(16, 4096, 4096), (8, 4096, 11008), (13, 2048, 1024)])
+def test_gemm_staged_activations_bitwise(M, N, K):
+    """The decode GEMM with its activations staged through LDS as whole rows
+    (XS) feeds the MFMAs the same operands as the direct fragment loads: the
+    results are bitwise equal (forced through the tuning knob)."""
+    import os
+    torch = G.torch()
+    hs = _hs()
+    rng = np.random.default_rng(M + N + K)
+    X = gen.round_to_bf16(rng.standard_normal((M, K)).astype(np.float32))
+    Wt = gen.round_to_bf16((rng.standard_normal((N, K)) * 0.05).astype(np.float32))
+    R = gen.round_to_bf16(rng.standard_normal((M, N)).astype(np.float32))
+    dX = G.to_dev_bf16(X)
+    dW = torch.from_numpy(G.tile_bits(gen.to_bf16_bits(Wt)).view(np.int16)).cuda()
+    outs = []
+    old = os.environ.get("HS_SKINNY_CFG")
+    try:
+        for xs in (0, 1):
+            os.environ["HS_SKINNY_CFG"] = f"1,1,16,{xs}"
+            Y = G.to_dev_bf16(R)
+            hs.hs_k_gemm(dX.data_ptr(), K, dW.data_ptr(), Y.data_ptr(), N, Y.data_ptr(), N,
+                         M, N, K, "resid", G.stream_ptr())
+            torch.cuda.synchronize()
+            outs.append(G.from_dev_bf16(Y))
+    finally:
+        if old is None:
+            os.environ.pop("HS_SKINNY_CFG", None)
+        else:
+            os.environ["HS_SKINNY_CFG"] = old
+    assert np.array_equal(outs[0], outs[1])
+    ref = R + X.astype(np.float64) @ Wt.astype(np.float64).T
+    assert np.abs(outs[1] - ref).max() <= 8e-3 * np.abs(ref).max()
+
+
 # 7B-shape projections at a 512-token prompt: few output tiles, so their k
 # ranges are split across workgroups (stream-K). Rows are sampled for the
 # float64 reference; two calls must agree bitwise.
