@@ -86,8 +86,16 @@ def log(*a):
 
 
 def _sha(path):
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    """SHA-256 of a kernel source's code: comments and blank lines removed and
+    runs of whitespace collapsed, so that a counter summary stays valid across
+    edits of the text around the code but not across any change to it."""
+    import re
+    with open(path, encoding="utf-8") as f:
+        src = f.read()
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", "", src)
+    lines = [" ".join(l.split()) for l in src.splitlines()]
+    return hashlib.sha256("\n".join(l for l in lines if l).encode()).hexdigest()
 
 
 def traffic_from_profiles(kernel, workload=None):

@@ -670,9 +670,9 @@ __global__ __launch_bounds__(64 * WV) void gemm_skinny(GemmArgs a) {
   const int r8 = fr % 8;
   // 16-byte position of lane (fr, g)'s row inside the 2 KiB image of a 16-row tile
   const int fpos = (fr / 8) * 64 + r8 * 8;
-  // activation rows: XS, load i = 2 c + h (instruction h of token chunk c):
-  // token 8 i + L / 8 from chunk (L % 8) ^ (L / 8) on; otherwise load c: token
-  // 16 c + fr (the chunk offset added per load)
+  // activation rows. XS: load i = 2 c + h (instruction h of token chunk c)
+  // reads token 8 i + L / 8, at 16-byte chunk (L % 8) ^ (L / 8) of each slab;
+  // otherwise load c reads token 16 c + fr (its chunk offset added per load)
   constexpr int XH = XS ? 2 : 1;
   const int xr = lane >> 3, xc = (lane & 7) ^ (lane >> 3);
   const bf16_t* xrow[MCH * XH];
