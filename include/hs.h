@@ -403,7 +403,8 @@ hs_status hs_kv_blob_describe(const void* host_blob, uint64_t avail,
  * sites named by hs_stage_set_timing_sites (a comma-separated list of
  * "embed", "attn_norm", "qkv" (the QKV projection with RoPE and the KV
  * append), "attn", "o_proj", "ffn_norm", "gate_up", "down", "final_norm",
- * "lm_head", "argmax", "kv_copy"; NULL or
+ * "lm_head", "argmax", "kv_copy"; a per-layer site followed by "@<layer>",
+ * e.g. "gate_up@12", names that layer's launch only; NULL or
  * "" = every site). Events between back-to-back kernels cost time of their
  * own, so timing a few sites disturbs a step less than timing all of them.
  * hs_stage_read_timing waits for the stage, then reports per (kernel, launch

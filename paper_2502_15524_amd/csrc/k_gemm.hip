@@ -202,9 +202,9 @@ __device__ __forceinline__ int chunk_pos(int r, int c) {
 
 // Multiply one stage (BK/32 steps of 32 k). Fragment reads are software
 // pipelined against the MFMAs and the order is pinned with scheduling group
-// barriers: the A fragment of row tile i+1 is read while the TM MFMAs of row
-// tile i run, and the B fragments of the next 32-k step are read during the
-// last row tile of the current one. The last row tile of a stage is deferred
+// barriers: the A fragment of row tile i + PD is read while the TM MFMAs of
+// row tile i run, and the B fragments of the next 32-k step are read with the
+// first A fragment that needs them. The last row tile of a stage is deferred
 // past the workgroup barrier: it runs while the next stage's first fragments
 // come from LDS (its operands are already in registers).
 template <int CPR>
@@ -212,57 +212,72 @@ __device__ __forceinline__ bf16x8_v lds_frag(const bf16_t* s, int r, int c) {
   return as_bf16x8(ld16(s + (r * CPR + chunk_pos<CPR>(r, c)) * 8));
 }
 
-template <int BN, int BM, int BK, int NS, int NW, int TN, int TM, typename Dma>
-__device__ __forceinline__ void ring_stage(f32x4_v (&acc)[TN][TM], bf16x8_v (&a)[2],
+// How many row tiles ahead of its MFMAs a wave reads the A fragments: three
+// for the 4- and 6-row-tile wave tiles (128 x 128 and 192-row tiles; 512-token
+// 7B shapes, MI355X: gate/up 96.6 -> 94.0 us, QKV 55.8 -> 53.8, o 29.3 ->
+// 28.2), one for the 8-row-tile ones of 256-row tiles (three made 8192-token
+// launches 1-4 % slower). The fragments and MFMAs are the same either way.
+template <int TN>
+constexpr int ring_pd() {
+  return (TN == 4 || TN == 6) ? 3 : 1;
+}
+
+template <int BN, int BM, int BK, int NS, int NW, int TN, int TM, int PD, typename Dma>
+__device__ __forceinline__ void ring_stage(f32x4_v (&acc)[TN][TM], bf16x8_v (&a)[PD + 1],
                                            bf16x8_v (&b)[2][TM], const bf16_t* sw,
                                            const bf16_t* sx, int wn, int wm, int fr, int g,
                                            bool pending, Dma&& dma) {
   using T = RTile<BN, BM, BK, NS, NW>;
-  constexpr int CPR = T::CPR, KS = BK / 32;
+  constexpr int CPR = T::CPR, KS = BK / 32, NT = TN * KS;
   constexpr int MASK_MFMA = 0x008, MASK_DS_READ = 0x100;
   // 256 x 256 tiles: a wave runs its MFMA groups at raised priority, so the
   // SIMD's other wave issues its LDS reads and loads in between instead of
   // competing with them (8192 tokens, MI355X: gate/up 1155-1162 -> 1107-1113
   // us, down 580 -> 562; the smaller tiles gained nothing)
   constexpr bool PRIO = BN == 256 && BM == 256 && NW == 8;
-  static_assert(TN % 2 == 0 && KS == 2, "the deferred row tile uses a[1] and b[1]");
+  // row tile t of the stage (t = ks TN + i) uses A slot t mod (PD + 1); the
+  // deferred last one must not share a slot with the next stage's first PD
+  static_assert(KS == 2 && NT % (PD + 1) == 0, "A fragment slots");
+  constexpr int LAST = (NT - 1) % (PD + 1);
+  auto read_a = [&](int t) {
+    a[t % (PD + 1)] = lds_frag<CPR>(sw, wn * T::WN + (t % TN) * 16 + fr, (t / TN) * 4 + g);
+  };
 #pragma unroll
   for (int j = 0; j < TM; ++j) b[0][j] = lds_frag<CPR>(sx, wm * T::WM + j * 16 + fr, g);
-  a[0] = lds_frag<CPR>(sw, wn * T::WN + fr, g);
-  __builtin_amdgcn_sched_group_barrier(MASK_DS_READ, TM + 1, 0);
+#pragma unroll
+  for (int t = 0; t < PD; ++t) read_a(t);
+  __builtin_amdgcn_sched_group_barrier(MASK_DS_READ, TM + PD, 0);
   // the previous stage's last row tile (operands in registers) runs while
   // this stage's first fragments are on their way from LDS
   if (pending) {
 #pragma unroll
     for (int j = 0; j < TM; ++j)
-      acc[TN - 1][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[1], b[1][j], acc[TN - 1][j], 0, 0, 0);
+      acc[TN - 1][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[LAST], b[1][j], acc[TN - 1][j], 0, 0, 0);
     __builtin_amdgcn_sched_group_barrier(MASK_MFMA, TM, 0);
   }
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
-    const int c = ks * 4 + g;
-#pragma unroll
-    for (int i = 0; i < TN; ++i) {
-      const int cur = i & 1, nxt = cur ^ 1;
-      dma(ks * TN + i);
-      if (i + 1 < TN) {
-        a[nxt] = lds_frag<CPR>(sw, wn * T::WN + (i + 1) * 16 + fr, c);
-      } else if (ks + 1 < KS) {
-#pragma unroll
-        for (int j = 0; j < TM; ++j)
-          b[(ks + 1) & 1][j] = lds_frag<CPR>(sx, wm * T::WM + j * 16 + fr, c + 4);
-        a[nxt] = lds_frag<CPR>(sw, wn * T::WN + fr, c + 4);
-      }
-      if (ks + 1 == KS && i + 1 == TN) break;  // deferred to the next stage (or the end)
-      if constexpr (PRIO) __builtin_amdgcn_s_setprio(1);
+  for (int t = 0; t < NT; ++t) {
+    const int ks = t / TN, i = t % TN;
+    dma(t);
+    // A of row tile t + PD; the B fragments of the next 32-k step together
+    // with the A fragment that first needs them
+    const bool ra = t + PD < NT, rb = ks + 1 < KS && i == TN - PD;
+    if (ra) read_a(t + PD);
+    if (rb) {
 #pragma unroll
       for (int j = 0; j < TM; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[cur], b[ks & 1][j], acc[i][j], 0, 0, 0);
-      if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
-      if (i + 1 < TN) __builtin_amdgcn_sched_group_barrier(MASK_DS_READ, 1, 0);
-      else if (ks + 1 < KS) __builtin_amdgcn_sched_group_barrier(MASK_DS_READ, TM + 1, 0);
-      __builtin_amdgcn_sched_group_barrier(MASK_MFMA, TM, 0);
+        b[(ks + 1) & 1][j] = lds_frag<CPR>(sx, wm * T::WM + j * 16 + fr, (ks + 1) * 4 + g);
     }
+    if (t == NT - 1) break;  // deferred to the next stage (or the end)
+    if constexpr (PRIO) __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+    for (int j = 0; j < TM; ++j)
+      acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[t % (PD + 1)], b[ks & 1][j], acc[i][j], 0, 0, 0);
+    if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
+    if (ra && rb) __builtin_amdgcn_sched_group_barrier(MASK_DS_READ, TM + 1, 0);
+    else if (ra) __builtin_amdgcn_sched_group_barrier(MASK_DS_READ, 1, 0);
+    else if (rb) __builtin_amdgcn_sched_group_barrier(MASK_DS_READ, TM, 0);
+    __builtin_amdgcn_sched_group_barrier(MASK_MFMA, TM, 0);
   }
 }
 
@@ -453,13 +468,14 @@ void gemm_ring(GemmArgs a, GemmSched sc) {
       else wait_vm<0>();
     }
     wg_barrier();
-    bf16x8_v fa[2], fb[2][TM];
+    constexpr int PD = ring_pd<TN>();
+    bf16x8_v fa[PD + 1], fb[2][TM];
     for (int j = 0; j < n; ++j) {
       const bool more_w = j + AW < n, more_x = j + AX < n;
       const bf16_t* sw = reinterpret_cast<const bf16_t*>(smem + (j % NS) * T::W_BYTES);
       const bf16_t* sx =
           reinterpret_cast<const bf16_t*>(smem + NS * T::W_BYTES + (j % NSX) * X_BYTES);
-      ring_stage<BN, BM, BK, NS, NW>(acc, fa, fb, sw, sx, wn, wm, fr, g, j > 0, [&](int step) {
+      ring_stage<BN, BM, BK, NS, NW, TN, TM, PD>(acc, fa, fb, sw, sx, wn, wm, fr, g, j > 0, [&](int step) {
         issue_part(j, step, more_w, more_x);
       });
       if constexpr (AW == AX) {
@@ -474,7 +490,7 @@ void gemm_ring(GemmArgs a, GemmSched sc) {
     // the last stage's deferred row tile
 #pragma unroll
     for (int jj = 0; jj < TM; ++jj)
-      acc[TN - 1][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[1], fb[1][jj], acc[TN - 1][jj], 0, 0, 0);
+      acc[TN - 1][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[(2 * TN - 1) % (PD + 1)], fb[1][jj], acc[TN - 1][jj], 0, 0, 0);
   };
 
   auto epilogue = [&](int n0, int m0) {

@@ -137,7 +137,8 @@ struct hs_stage {
   std::vector<Xfer> xfer;
 
   bool timing = false;
-  std::string timing_sites;  // ",site,site," or empty for every site
+  std::string timing_sites;  // ",site,site@layer," or empty for every site
+  int cur_layer = -1;        // decoder layer being enqueued (-1: none)
   std::vector<Pending> pending;
   std::map<std::string, Stat> stats;
   std::vector<hipEvent_t> ev_pool;
@@ -220,7 +221,10 @@ bool timed_site(const hs_stage* st, const char* site) {
   if (!st->timing) return false;
   if (st->timing_sites.empty()) return true;
   const std::string key = std::string(",") + site + ",";
-  return st->timing_sites.find(key) != std::string::npos;
+  if (st->timing_sites.find(key) != std::string::npos) return true;
+  if (st->cur_layer < 0) return false;
+  const std::string one = std::string(",") + site + "@" + std::to_string(st->cur_layer) + ",";
+  return st->timing_sites.find(one) != std::string::npos;
 }
 
 template <typename F>
@@ -387,7 +391,17 @@ struct LayerCall {
   double kv_read_bytes;
 };
 
+hs_status layer_forward_(hs_stage* st, int l, bf16_t* x, const LayerCall& c, hipStream_t s);
+
+// One decoder layer, with the layer recorded for layer-qualified timing sites.
 hs_status layer_forward(hs_stage* st, int l, bf16_t* x, const LayerCall& c, hipStream_t s) {
+  st->cur_layer = l;
+  const hs_status r = layer_forward_(st, l, x, c, s);
+  st->cur_layer = -1;
+  return r;
+}
+
+hs_status layer_forward_(hs_stage* st, int l, bf16_t* x, const LayerCall& c, hipStream_t s) {
   const hs_model_cfg& m = st->cfg;
   const LayerSlots& ls = st->L.layers[l - st->rb];
   const int H = m.hidden, D = m.head_dim, F = m.ffn;

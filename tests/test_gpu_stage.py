@@ -448,8 +448,8 @@ def test_error_paths(env):
 
 def test_timing_sites_filter(env):
     """Timing every site reports every kernel of the forward pass; naming
-    sites reports only their launches (one per layer), and results do not
-    depend on timing."""
+    sites reports only their launches (one per layer, or one layer's with
+    "site@layer"), and results do not depend on timing."""
     hs = env["hs"]
     st = make(env, 0, 2)
     hs.hs_stage_read_timing(st.h)
@@ -464,9 +464,14 @@ def test_timing_sites_filter(env):
     two = hs.hs_stage_read_timing(st.h)
     assert {s["site"] for s in two} == {"qkv", "down"}
     assert all(s["launches"] == CFG.n_layers and s["total_ms"] > 0 for s in two)
+    # "site@layer" names one layer's launch; a layer outside the stage names none
+    hs.hs_stage_set_timing_sites(st.h, "gate_up@1,qkv@7,lm_head@1")
+    h_one = _hidden_prefill_full(st, env["prompt"], seq_id=3)
+    one = hs.hs_stage_read_timing(st.h)
+    assert [(s["site"], s["launches"]) for s in one] == [("gate_up", 1)]
     hs.hs_stage_set_timing(st.h, 0)
     hs.hs_stage_set_timing_sites(st.h, None)
-    assert np.array_equal(h_all, h_two)
+    assert np.array_equal(h_all, h_two) and np.array_equal(h_all, h_one)
 
 
 def _hidden_prefill_full(st, tokens, seq_id):
