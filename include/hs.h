@@ -224,7 +224,9 @@ hs_status hs_stage_invalidate_weights(hs_stage* st);
  * them; seq_lens (host, each >= 1) give their prompt lengths; the total T
  * must not exceed max_batch_tokens, and each length max_ctx.
  *  in  : stage starts at layer 0 -> device int32 token ids [T];
- *        otherwise device bf16 hidden states [T][hidden].
+ *        otherwise device bf16 hidden states [T][hidden], read in place
+ *        by the stage's first layer (it may be `out` itself; otherwise the
+ *        two must not overlap).
  *        Tokens and rows are packed sequence after sequence.
  *  out : stage ends at the last layer -> device int32 [n_seqs], the greedy
  *        next token of each sequence (lowest index among equal maxima);
@@ -244,7 +246,8 @@ hs_status hs_stage_prefill(hs_stage* st, int32_t n_seqs, const int64_t* seq_ids,
 /* One decode step for `n_seqs` live sequences (host seq_ids, distinct):
  * each gets one new position appended to its KV cache.
  *  in  : first stage -> device int32 [n_seqs] token ids; otherwise device
- *        bf16 [n_seqs][hidden].
+ *        bf16 [n_seqs][hidden] (as for prefill: read in place, `out` or
+ *        not overlapping it).
  *  out : last stage -> device int32 [n_seqs] next tokens; otherwise device
  *        bf16 [n_seqs][hidden].
  *  logits_opt : as for prefill.

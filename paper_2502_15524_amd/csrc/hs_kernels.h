@@ -123,6 +123,11 @@ int argmax_chunks(int n_cols);
 hipError_t argmax_rows(const float* logits, int n_rows, int n_cols, int32_t* part, int32_t* out,
                        hipStream_t s, LaunchInfo* info);
 
+// Copy `n` int32 values (n % 4 == 0, both pointers 16-byte aligned) from
+// pinned host memory to device memory with system-coherent loads: the
+// per-call metadata of a stage, pulled by a kernel at the start of the call.
+hipError_t meta_pull(const int32_t* host, int32_t* dev, int64_t n, hipStream_t s);
+
 // Copy `n_units` KV units (a K block followed by its V block, unit_bytes each);
 // slots at or past valid[u] are written as zero when zero_tail is set.
 hipError_t kv_copy(const uint64_t* src, const uint64_t* dst, const int32_t* valid, int n_units,

@@ -90,8 +90,14 @@ struct hs_stage {
 
   std::vector<hipStream_t> copy;
   int next_copy = 0;
+  // Completion of the latest call: the event its end recorded (own_done, or
+  // the metadata slot's event of a call that used one: one event record per
+  // call, each costing a fence on the stream).
+  hipEvent_t own_done = nullptr;
   hipEvent_t last_done = nullptr;
   bool last_valid = false;
+  hipStream_t last_stream = nullptr;
+  int cur_meta = -1;  // metadata slot of the call in progress
 
   std::map<uint64_t, Chunk> chunks;
   std::vector<char> layer_landed;
@@ -164,7 +170,7 @@ hs_stage::~hs_stage() {
   if (desc_ev) (void)hipEventDestroy(desc_ev);
   if (h_desc) (void)hipHostFree(h_desc);
   if (d_desc) (void)hipFree(d_desc);
-  if (last_done) (void)hipEventDestroy(last_done);
+  if (own_done) (void)hipEventDestroy(own_done);
   for (auto s : copy) (void)hipStreamDestroy(s);
   for (auto& x : xfer) (void)hipEventDestroy(x.ev);
   if (d_stage) (void)hipFree(d_stage);
@@ -182,16 +188,40 @@ namespace {
 // Work goes on the caller's stream; NULL is the null stream.
 hipStream_t pick(hs_stage*, void* stream) { return static_cast<hipStream_t>(stream); }
 
+// A call on another stream than the previous one waits for that call; on the
+// same stream the order is implicit.
 hs_status begin_call(hs_stage* st, hipStream_t s) {
-  if (st->last_valid) HIPTRY(hipStreamWaitEvent(s, st->last_done, 0));
+  if (st->last_valid && s != st->last_stream) HIPTRY(hipStreamWaitEvent(s, st->last_done, 0));
   return HS_OK;
 }
 
+// Record the call's completion; a call that pulled metadata records its
+// slot's event, which then guards both the slot's reuse and the next call.
 hs_status end_call(hs_stage* st, hipStream_t s) {
-  HIPTRY(hipEventRecord(st->last_done, s));
+  hipEvent_t e = st->cur_meta >= 0 ? st->meta_ev[st->cur_meta] : st->own_done;
+  st->cur_meta = -1;
+  HIPTRY(hipEventRecord(e, s));
+  st->last_done = e;
   st->last_valid = true;
+  st->last_stream = s;
   return HS_OK;
 }
+
+// Ends a call that pulled metadata on every path: an error return after the
+// pull still records the slot's event, so the host never rewrites a slot that
+// a queued pull may read.
+struct CallEnd {
+  hs_stage* st;
+  hipStream_t s;
+  bool armed = true;
+  ~CallEnd() {
+    if (armed) (void)end_call(st, s);
+  }
+  hs_status finish() {
+    armed = false;
+    return end_call(st, s);
+  }
+};
 
 hipEvent_t pool_event(hs_stage* st) {
   if (!st->ev_pool.empty()) {
@@ -284,11 +314,14 @@ hs_status meta_acquire(hs_stage* st, Meta* m) {
   return HS_OK;
 }
 
+// Pull the call's metadata into device memory; the slot's event is recorded
+// when the call ends (end_call).
 hs_status meta_upload(hs_stage* st, const Meta& m, hipStream_t s) {
   if (m.overflow || m.used * 4 > st->meta_bytes) return fail(HS_EINVAL, "internal: metadata overflow");
-  HIPTRY(hipMemcpyAsync(m.d, m.h, m.used * 4, hipMemcpyHostToDevice, s));
-  HIPTRY(hipEventRecord(st->meta_ev[m.slot], s));
+  st->cur_meta = m.slot;
   st->meta_used[m.slot] = true;
+  const hipError_t e = meta_pull(m.h, m.d, (int64_t)m.used, s);
+  if (e != hipSuccess) return fail(HS_EHIP, hip_msg("metadata pull", e));
   return HS_OK;
 }
 
@@ -379,9 +412,13 @@ bf16_t* pool(const hs_stage* st, int layer) {
 int32_t blocks_for(int32_t n) { return (n + kBlock - 1) / kBlock; }
 
 // One decoder layer on rows [0, T) of x (bf16 residual stream, in place).
+// The stage's first layer reads its residual stream from xin (the caller's
+// input, or x itself) and writes x, so an input in another buffer is never
+// copied first.
 struct LayerCall {
   bool decode;
   int T;
+  const bf16_t* xin;
   const int32_t *pos, *slot;             // device
   const int32_t *cu, *tiles;             // prefill
   int n_tiles, attn_waves;
@@ -410,16 +447,17 @@ hs_status layer_forward_(hs_stage* st, int l, bf16_t* x, const LayerCall& c, hip
   // Up to 16 tokens (decode batches) the skinny GEMMs apply the two norms
   // themselves and read the residual stream directly.
   const bool fuse_norm = c.T <= 16;
+  const bf16_t* xr = l == st->begin ? c.xin : x;  // residual stream before the o projection
   hs_status r;
   if (!fuse_norm) {
     r = run(st, s, "attn_norm", [&](LaunchInfo* i) {
-      return rmsnorm(x, H, nullptr, c.T, H, W(st, ls.attn_norm), m.rms_eps, st->w_u, H, s, i);
+      return rmsnorm(xr, H, nullptr, c.T, H, W(st, ls.attn_norm), m.rms_eps, st->w_u, H, s, i);
     });
     if (r != HS_OK) return r;
   }
   r = run(st, s, "qkv", [&](LaunchInfo* i) {
     GemmArgs g = fuse_norm
-                     ? gemm_args(st, x, H, W(st, ls.qkv), st->w_qkv, NQKV, nullptr, 0, c.T, NQKV, H)
+                     ? gemm_args(st, xr, H, W(st, ls.qkv), st->w_qkv, NQKV, nullptr, 0, c.T, NQKV, H)
                      : gemm_args(st, st->w_u, H, W(st, ls.qkv), st->w_qkv, NQKV, nullptr, 0, c.T, NQKV, H);
     if (fuse_norm) g.norm_gain = W(st, ls.attn_norm), g.norm_eps = m.rms_eps;
     // the image stores q and k heads with their RoPE halves interleaved
@@ -457,7 +495,7 @@ hs_status layer_forward_(hs_stage* st, int l, bf16_t* x, const LayerCall& c, hip
   }
   if (r != HS_OK) return r;
   r = run(st, s, "o_proj", [&](LaunchInfo* i) {
-    GemmArgs g = gemm_args(st, st->w_attn, QD, W(st, ls.o), x, H, x, H, c.T, H, QD);
+    GemmArgs g = gemm_args(st, st->w_attn, QD, W(st, ls.o), x, H, xr, H, c.T, H, QD);
     return gemm(g, EPI_RESID, s, i);
   });
   if (r != HS_OK) return r;
@@ -864,7 +902,7 @@ extern "C" hs_status hs_stage_create(const hs_model_cfg* cfg, int32_t layer_begi
       return bail(fail(HS_EHIP, "stream creation failed"));
     st->copy.push_back(s);
   }
-  if (hipEventCreateWithFlags(&st->last_done, hipEventDisableTiming) != hipSuccess ||
+  if (hipEventCreateWithFlags(&st->own_done, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&st->desc_ev, hipEventDisableTiming) != hipSuccess)
     return bail(fail(HS_EHIP, "event creation failed"));
 
@@ -876,7 +914,7 @@ extern "C" hs_status hs_stage_create(const hs_model_cfg* cfg, int32_t layer_begi
     st->meta_bytes = ((std::max(pre, dec) + 64 * 8) * 4 + 4095) / 4096 * 4096;
     for (int i = 0; i < kRing; ++i) {
       if (hipHostMalloc(reinterpret_cast<void**>(&st->h_meta[i]), st->meta_bytes,
-                        hipHostMallocDefault) != hipSuccess ||
+                        hipHostMallocCoherent) != hipSuccess ||
           hipMalloc(reinterpret_cast<void**>(&st->d_meta[i]), st->meta_bytes) != hipSuccess)
         return bail(fail(HS_ENOMEM, "metadata buffer allocation failed"));
       if (hipEventCreateWithFlags(&st->meta_ev[i], hipEventDisableTiming) != hipSuccess)
@@ -1059,6 +1097,7 @@ extern "C" hs_status hs_stage_prefill(hs_stage* st, int32_t n, const int64_t* id
 
   r = begin_call(st, s);
   if (r != HS_OK) return r;
+  CallEnd ce{st, s};
   r = meta_upload(st, mt, s);
   if (r != HS_OK) return r;
 
@@ -1072,12 +1111,11 @@ extern "C" hs_status hs_stage_prefill(hs_stage* st, int32_t n, const int64_t* id
                    x, s, i);
     });
     if (r != HS_OK) return r;
-  } else if (in != x) {
-    HIPTRY(hipMemcpyAsync(x, in, (size_t)T * H * 2, hipMemcpyDeviceToDevice, s));
   }
   LayerCall c{};
   c.decode = false;
   c.T = (int)T;
+  c.xin = first ? x : static_cast<const bf16_t*>(in);
   c.pos = d_pos;
   c.slot = d_slot;
   c.cu = d_cu;
@@ -1099,7 +1137,7 @@ extern "C" hs_status hs_stage_prefill(hs_stage* st, int32_t n, const int64_t* id
   }
   st->free_blocks.resize(free_end);
   for (int i = 0; i < n; ++i) st->seqs.emplace(ids[i], std::move(fresh[i]));
-  return end_call(st, s);
+  return ce.finish();
   ABI_END
 }
 
@@ -1165,6 +1203,7 @@ extern "C" hs_status hs_stage_decode(hs_stage* st, int32_t n, const int64_t* ids
   }
   r = begin_call(st, s);
   if (r != HS_OK) return r;
+  CallEnd ce{st, s};
   r = meta_upload(st, mt, s);
   if (r != HS_OK) return r;
 
@@ -1177,12 +1216,11 @@ extern "C" hs_status hs_stage_decode(hs_stage* st, int32_t n, const int64_t* ids
       return embed(static_cast<const int32_t*>(in), W(st, st->L.embed), st->cfg.vocab, H, n, x, s, i);
     });
     if (r != HS_OK) return r;
-  } else if (in != x) {
-    HIPTRY(hipMemcpyAsync(x, in, (size_t)n * H * 2, hipMemcpyDeviceToDevice, s));
   }
   LayerCall c{};
   c.decode = true;
   c.T = n;
+  c.xin = first ? x : static_cast<const bf16_t*>(in);
   c.pos = d_pos;
   c.slot = d_slot;
   c.bt = d_bt;
@@ -1207,7 +1245,7 @@ extern "C" hs_status hs_stage_decode(hs_stage* st, int32_t n, const int64_t* ids
     if (new_block[i] >= 0) sq[i]->blocks.push_back(new_block[i]);
     sq[i]->n_tokens += 1;
   }
-  return end_call(st, s);
+  return ce.finish();
   ABI_END
 }
 
