@@ -72,6 +72,10 @@ def parse():
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="summarise two rocprofv3 counter passes over a --traffic-probe run "
                          "(no GPU work)")
+    ap.add_argument("--gemm-shapes", action="store_true",
+                    help="time the projection GEMMs of the 7B and 8B-GQA shapes through the "
+                         "kernel entry point beside torch.matmul (hipBLASLt) on the same "
+                         "shapes; prints a markdown table")
     ap.add_argument("--no-extras", action="store_true",
                     help="headline workload only")
     ap.add_argument("--extras", default=",".join(EXTRAS),
@@ -220,6 +224,8 @@ def main():
     from workloads import WORKLOADS
 
     assert torch.cuda.is_available()
+    if args.gemm_shapes:
+        return gemm_shapes()
     if args.workload.endswith("scale-down"):
         res = bench_scale_down(WORKLOADS[args.workload], args)
     elif args.workload != "7b-stage8-15-cold":
@@ -238,6 +244,77 @@ def main():
                     WORKLOADS["8b-4x8-ragged-merge"], args, n_dec=256, oracle_sample=True)
     if res is not None:
         print(json.dumps(res), flush=True)
+
+
+def gemm_shapes(reps=20, copies=4):
+    """The decoder-layer projections of the 7B shape at 512 and 8192 prompt
+    tokens and at 1 and 8 decode tokens, and of the 8B-GQA shape at 16 decode
+    tokens, each timed with HIP events over `reps` launches through
+    hs_k_gemm (the library picks the configuration as in a stage) with
+    `copies` weight matrices in rotation, so the weights stream from HBM as in
+    a stage; beside them torch.matmul (hipBLASLt) of the same operands, which
+    writes the plain product (no residual read, no SwiGLU halving). Random
+    bf16 operands (timing only). QKV runs with the plain-store epilogue here;
+    in a stage, prompts of more than 64 tokens rotate and append in the QKV
+    epilogue and decode batches fold the RMSNorm into QKV and gate/up."""
+    import torch
+    from paper_2502_15524_amd import hs
+    from workloads import MODELS
+    dev = "cuda"
+    rows = []
+    for model, Ms in (("llama2-7b", (512, 8192, 1, 8)), ("llama3-8b", (16,))):
+        cfg = MODELS[model]
+        H, F, D = cfg.hidden, cfg.ffn, cfg.head_dim
+        projs = (("qkv", (cfg.n_heads + 2 * cfg.n_kv_heads) * D, H, 0),
+                 ("o", H, cfg.n_heads * D, 1), ("gate/up", 2 * F, H, 2), ("down", H, F, 1))
+        for M in Ms:
+            for name, N, K, epi in projs:
+                kp = (K + 63) // 64 * 64
+                X = torch.zeros(M, kp, device=dev, dtype=torch.bfloat16)
+                X[:, :K] = torch.randn(M, K, device=dev).bfloat16()
+                Ws = [(torch.randn(N, K, device=dev) * 0.02).bfloat16() for _ in range(copies)]
+                ncol = N // 2 if epi == 2 else N
+                Y = torch.zeros(M, ncol, device=dev, dtype=torch.bfloat16)
+                R = torch.randn(M, ncol, device=dev).bfloat16()
+                it = [0]
+
+                def ours():
+                    W = Ws[it[0] % copies]
+                    it[0] += 1
+                    hs.hs_k_gemm(X.data_ptr(), kp, W.data_ptr(), Y.data_ptr(), ncol,
+                                 R.data_ptr() if epi == 1 else 0, ncol, M, N, K, epi, 0)
+
+                def theirs():
+                    W = Ws[it[0] % copies]
+                    it[0] += 1
+                    torch.matmul(X[:, :K], W.t())
+
+                res = []
+                for fn in (ours, theirs):
+                    for _ in range(3):
+                        fn()
+                    e0 = torch.cuda.Event(enable_timing=True)
+                    e1 = torch.cuda.Event(enable_timing=True)
+                    torch.cuda.synchronize()
+                    e0.record()
+                    for _ in range(reps):
+                        fn()
+                    e1.record()
+                    torch.cuda.synchronize()
+                    res.append(e0.elapsed_time(e1) / reps * 1e3)
+                flops = 2.0 * M * N * K
+                wbytes = 2.0 * N * K
+                rows.append(f"| {model} | {M} | {name} | {N} x {K} | {res[0]:.1f} | "
+                            f"{flops / res[0] / 1e6:.0f} | {wbytes / res[0] / 1e3:.0f} | "
+                            f"{res[1]:.1f} | {flops / res[1] / 1e6:.0f} |")
+                log(rows[-1])
+                del Ws, X, Y, R
+    print("| model | tokens | projection | N x K | hs_k_gemm us | TFLOP/s | weight GB/s | "
+          "torch.matmul us | TFLOP/s |")
+    print("|---|---|---|---|---|---|---|---|---|")
+    for r in rows:
+        print(r)
+    return None
 
 
 def bench_c2(args):
