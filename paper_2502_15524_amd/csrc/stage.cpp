@@ -96,7 +96,6 @@ struct hs_stage {
   hipEvent_t own_done = nullptr;
   hipEvent_t last_done = nullptr;
   bool last_valid = false;
-  hipStream_t last_stream = nullptr;
   int cur_meta = -1;  // metadata slot of the call in progress
 
   std::map<uint64_t, Chunk> chunks;
@@ -188,10 +187,10 @@ namespace {
 // Work goes on the caller's stream; NULL is the null stream.
 hipStream_t pick(hs_stage*, void* stream) { return static_cast<hipStream_t>(stream); }
 
-// A call on another stream than the previous one waits for that call; on the
-// same stream the order is implicit.
+// Every call waits for the previous one, so calls on different streams stay
+// ordered (on the same stream the wait costs nothing measurable).
 hs_status begin_call(hs_stage* st, hipStream_t s) {
-  if (st->last_valid && s != st->last_stream) HIPTRY(hipStreamWaitEvent(s, st->last_done, 0));
+  if (st->last_valid) HIPTRY(hipStreamWaitEvent(s, st->last_done, 0));
   return HS_OK;
 }
 
@@ -203,7 +202,6 @@ hs_status end_call(hs_stage* st, hipStream_t s) {
   HIPTRY(hipEventRecord(e, s));
   st->last_done = e;
   st->last_valid = true;
-  st->last_stream = s;
   return HS_OK;
 }
 
