@@ -164,7 +164,8 @@ def check_layer(cfg, W, layer, x_in, gpu_out, n_tok, head=False, tag=""):
 def test_7b_middle_stage_512_per_layer_and_cold_equals_warm():
     """Layers 8-15 of the 7B shape, one 512-token prompt (the benchmark's
     workload), fed the oracle's output of layers 0-7 on the prompt (bf16):
-    cold streaming == warm, 8 single-layer stages == the stage, every layer
+    cold streaming == warm == in place (input and output in one buffer),
+    8 single-layer stages == the stage, every layer
     against the oracle, KV through the export blob, the whole stage and two
     decode steps against the oracle end to end."""
     torch = G.torch()
@@ -201,6 +202,10 @@ def test_7b_middle_stage_512_per_layer_and_cold_equals_warm():
     torch.cuda.synchronize()
     warm = G.from_dev_bf16(out)
     assert np.array_equal(outs[0], warm) and np.array_equal(outs[1], warm)
+    inout = x.clone()                        # input and output in one buffer
+    st.prefill([3], [P], inout.data_ptr(), inout.data_ptr(), 0, sp)
+    torch.cuda.synchronize()
+    assert np.array_equal(G.from_dev_bf16(inout), warm)
     n = hs.hs_kv_export_size(st.h, [2])
     blob = torch.zeros(n, dtype=torch.uint8, device="cuda")
     hs.hs_kv_export(st.h, [2], blob.data_ptr(), n, sp)
@@ -210,8 +215,11 @@ def test_7b_middle_stage_512_per_layer_and_cold_equals_warm():
     for s in range(2):
         od = torch.zeros((1, cfg.hidden), dtype=torch.bfloat16, device="cuda")
         st.decode([2], G.to_dev_bf16(dec_in[s]).data_ptr(), od.data_ptr(), 0, sp)
+        io = G.to_dev_bf16(dec_in[s])        # the same step in place, on the twin sequence
+        st.decode([3], io.data_ptr(), io.data_ptr(), 0, sp)
         torch.cuda.synchronize()
         dec_out.append(G.from_dev_bf16(od))
+        assert np.array_equal(G.from_dev_bf16(io), dec_out[-1])
     st.close()
     img.close()
     say("single-layer stages")
