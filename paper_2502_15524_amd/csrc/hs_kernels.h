@@ -124,9 +124,11 @@ hipError_t argmax_rows(const float* logits, int n_rows, int n_cols, int32_t* par
                        hipStream_t s, LaunchInfo* info);
 
 // Copy `n` int32 values (n % 4 == 0, both pointers 16-byte aligned) from
-// pinned host memory to device memory with system-coherent loads: the
-// per-call metadata of a stage, pulled by a kernel at the start of the call.
-hipError_t meta_pull(const int32_t* host, int32_t* dev, int64_t n, hipStream_t s);
+// pinned host memory to device memory with system-coherent loads, and in the
+// same launch `n2` more from host2 to dev2 (same rules; n2 = 0: none): the
+// per-call metadata and copy descriptors of a stage, pulled by a kernel.
+hipError_t meta_pull(const int32_t* host, int32_t* dev, int64_t n, hipStream_t s,
+                     const int32_t* host2 = nullptr, int32_t* dev2 = nullptr, int64_t n2 = 0);
 
 // Copy `n_units` KV units (a K block followed by its V block, unit_bytes each);
 // slots at or past valid[u] are written as zero when zero_tail is set.

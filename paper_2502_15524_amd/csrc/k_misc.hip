@@ -16,25 +16,32 @@ namespace hs {
 // they see what the host wrote before the launch, never a cached copy of an
 // earlier call's values.
 
-__global__ __launch_bounds__(256) void meta_pull_kernel(const int32_t* host, int32_t* dev,
-                                                        int64_t n16) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+// Workgroups [0, b0) copy the first segment, the rest the second.
+__global__ __launch_bounds__(256) void meta_pull_kernel(const int32_t* h0, int32_t* d0,
+                                                        int64_t n0, const int32_t* h1,
+                                                        int32_t* d1, int64_t n1, int b0) {
+  const bool first = (int)blockIdx.x < b0;
+  const int64_t i = (int64_t)(first ? blockIdx.x : blockIdx.x - b0) * 256 + threadIdx.x;
+  const int64_t n16 = first ? n0 : n1;
   if (i >= n16) return;
   typedef unsigned u32x4_v __attribute__((ext_vector_type(4)));
   constexpr int kSystem = 1 | 16;  // sc0 | sc1
   const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<int32_t*>(host), 0, (int)(n16 * 16), 0x00020000);
+      const_cast<int32_t*>(first ? h0 : h1), 0, (int)(n16 * 16), 0x00020000);
   const u32x4_v v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)(i * 16), 0, kSystem);
-  *reinterpret_cast<u32x4_v*>(dev + i * 4) = v;
+  *reinterpret_cast<u32x4_v*>((first ? d0 : d1) + i * 4) = v;
 }
 
-hipError_t meta_pull(const int32_t* host, int32_t* dev, int64_t n, hipStream_t s) {
-  if (n <= 0) return hipSuccess;
-  if ((n % 4) || (((uintptr_t)host | (uintptr_t)dev) & 15) || n * 4 >= (1ll << 31))
+hipError_t meta_pull(const int32_t* host, int32_t* dev, int64_t n, hipStream_t s,
+                     const int32_t* host2, int32_t* dev2, int64_t n2) {
+  if (n < 0 || n2 < 0 || (n % 4) || (n2 % 4) || n * 4 >= (1ll << 31) || n2 * 4 >= (1ll << 31) ||
+      (n && (((uintptr_t)host | (uintptr_t)dev) & 15)) ||
+      (n2 && (((uintptr_t)host2 | (uintptr_t)dev2) & 15)))
     return hipErrorInvalidValue;
-  const int64_t n16 = n / 4;
-  hipLaunchKernelGGL(meta_pull_kernel, dim3((unsigned)((n16 + 255) / 256)), dim3(256), 0, s, host,
-                     dev, n16);
+  const int b0 = (int)((n / 4 + 255) / 256), b1 = (int)((n2 / 4 + 255) / 256);
+  if (b0 + b1 == 0) return hipSuccess;
+  hipLaunchKernelGGL(meta_pull_kernel, dim3((unsigned)(b0 + b1)), dim3(256), 0, s, host, dev,
+                     n / 4, host2, dev2, n2 / 4, b0);
   return hipGetLastError();
 }
 

@@ -96,7 +96,8 @@ struct hs_stage {
   hipEvent_t own_done = nullptr;
   hipEvent_t last_done = nullptr;
   bool last_valid = false;
-  int cur_meta = -1;  // metadata slot of the call in progress
+  int cur_meta = -1;      // metadata slot of the call in progress
+  bool cur_desc = false;  // the call in progress pulled copy descriptors
 
   std::map<uint64_t, Chunk> chunks;
   std::vector<char> layer_landed;
@@ -194,11 +195,15 @@ hs_status begin_call(hs_stage* st, hipStream_t s) {
   return HS_OK;
 }
 
-// Record the call's completion; a call that pulled metadata records its
-// slot's event, which then guards both the slot's reuse and the next call.
+// Record the call's completion; a call that pulled metadata or copy
+// descriptors records the event that guards that buffer's reuse, which then
+// also orders the next call.
 hs_status end_call(hs_stage* st, hipStream_t s) {
-  hipEvent_t e = st->cur_meta >= 0 ? st->meta_ev[st->cur_meta] : st->own_done;
+  hipEvent_t e = st->cur_meta >= 0 ? st->meta_ev[st->cur_meta]
+                 : st->cur_desc     ? st->desc_ev
+                                    : st->own_done;
   st->cur_meta = -1;
+  st->cur_desc = false;
   HIPTRY(hipEventRecord(e, s));
   st->last_done = e;
   st->last_valid = true;
@@ -568,7 +573,7 @@ hs_status desc_reserve(hs_stage* st, uint64_t n) {
   st->d_desc = nullptr;
   st->desc_cap = 0;
   const uint64_t cap = std::max<uint64_t>(need, 1 << 16);
-  if (hipHostMalloc(reinterpret_cast<void**>(&st->h_desc), cap, hipHostMallocDefault) != hipSuccess)
+  if (hipHostMalloc(reinterpret_cast<void**>(&st->h_desc), cap, hipHostMallocCoherent) != hipSuccess)
     return fail(HS_ENOMEM, "pinned descriptor buffer allocation failed");
   if (hipMalloc(reinterpret_cast<void**>(&st->d_desc), cap) != hipSuccess)
     return fail(HS_ENOMEM, "device descriptor buffer allocation failed");
@@ -581,8 +586,26 @@ struct Units {
   std::vector<int32_t> valid;
 };
 
+// Pull the descriptors (the first desc_bytes of the pinned buffer) into the
+// device descriptor buffer and the blob header, if any, straight into the
+// blob, with one kernel (a copy command costs a stream fence of its own).
+// Header sizes are multiples of 16 bytes (64 + 16 per sequence record).
+hs_status pull_desc(hs_stage* st, const uint8_t* h, uint64_t desc_bytes,
+                    const std::vector<uint8_t>* head, void* head_dst, hipStream_t s) {
+  const uint64_t hn = head ? head->size() : 0;
+  if (hn % 16) return fail(HS_EINVAL, "internal: blob header not a multiple of 16 bytes");
+  const hipError_t e = meta_pull(
+      reinterpret_cast<const int32_t*>(h), reinterpret_cast<int32_t*>(st->d_desc),
+      (int64_t)(desc_bytes / 4), s, reinterpret_cast<const int32_t*>(h + desc_bytes),
+      static_cast<int32_t*>(head_dst), (int64_t)(hn / 4));
+  if (e != hipSuccess) return fail(HS_EHIP, hip_msg("descriptor pull", e));
+  return HS_OK;
+}
+
 // Upload descriptors (and optionally a blob header, copied to head_dst in the
-// same upload) and launch the KV copy kernel on stream s.
+// same upload) and launch the KV copy kernel on stream s. The descriptor
+// buffer's guard event is recorded by the call's end_call (one upload per
+// call).
 hs_status copy_units(hs_stage* st, const Units& u, int zero_tail, hipStream_t s,
                      const std::vector<uint8_t>* head = nullptr, void* head_dst = nullptr) {
   const uint64_t n = u.src.size();
@@ -596,9 +619,8 @@ hs_status copy_units(hs_stage* st, const Units& u, int zero_tail, hipStream_t s,
   memcpy(h + o_dst, u.dst.data(), n * 8);
   memcpy(h + o_val, u.valid.data(), n * 4);
   if (head) memcpy(h + o_head, head->data(), head->size());
-  HIPTRY(hipMemcpyAsync(st->d_desc, h, o_head + hb, hipMemcpyHostToDevice, s));
-  if (head) HIPTRY(hipMemcpyAsync(head_dst, st->d_desc + o_head, head->size(),
-                                  hipMemcpyDeviceToDevice, s));
+  r = pull_desc(st, h, o_head, head, head_dst, s);
+  if (r != HS_OK) return r;
   const uint64_t* dsrc = reinterpret_cast<const uint64_t*>(st->d_desc);
   const uint64_t* ddst = reinterpret_cast<const uint64_t*>(st->d_desc + o_dst);
   const int32_t* dval = reinterpret_cast<const int32_t*>(st->d_desc + o_val);
@@ -609,7 +631,7 @@ hs_status copy_units(hs_stage* st, const Units& u, int zero_tail, hipStream_t s,
     });
     if (r != HS_OK) return r;
   }
-  HIPTRY(hipEventRecord(st->desc_ev, s));
+  st->cur_desc = true;
   st->desc_used = true;
   return HS_OK;
 }
@@ -629,9 +651,8 @@ hs_status desc_upload(hs_stage* st, const Units& u, hipStream_t s, const std::ve
   memcpy(h + o_dst, u.dst.data(), n * 8);
   memcpy(h + o_val, u.valid.data(), n * 4);
   if (head) memcpy(h + o_head, head->data(), head->size());
-  HIPTRY(hipMemcpyAsync(st->d_desc, h, o_head + hb, hipMemcpyHostToDevice, s));
-  if (head) HIPTRY(hipMemcpyAsync(head_dst, st->d_desc + o_head, head->size(),
-                                  hipMemcpyDeviceToDevice, s));
+  r = pull_desc(st, h, o_head, head, head_dst, s);
+  if (r != HS_OK) return r;
   *dsrc = reinterpret_cast<const uint64_t*>(st->d_desc);
   *ddst = reinterpret_cast<const uint64_t*>(st->d_desc + o_dst);
   *dval = reinterpret_cast<const int32_t*>(st->d_desc + o_val);
@@ -1358,9 +1379,10 @@ extern "C" hs_status hs_kv_export(hs_stage* st, int32_t n, const int64_t* ids, v
   hipStream_t s = pick(st, stream);
   r = begin_call(st, s);
   if (r != HS_OK) return r;
+  CallEnd ce{st, s};
   r = copy_units(st, u, 1, s, &head, dst);
   if (r != HS_OK) return r;
-  return end_call(st, s);
+  return ce.finish();
   ABI_END
 }
 
@@ -1373,6 +1395,7 @@ extern "C" hs_status hs_kv_import(hs_stage* st, const void* src, uint64_t bytes,
   hipStream_t s = pick(st, stream);
   hs_status r = begin_call(st, s);
   if (r != HS_OK) return r;
+  CallEnd ce{st, s};
   // one read covers the header and up to 256 sequence records; a blob with
   // more sequences takes a second read for the rest
   const uint64_t first = std::min<uint64_t>(bytes, kBlobHeader + kBlobRecord * 256);
@@ -1404,7 +1427,7 @@ extern "C" hs_status hs_kv_import(hs_stage* st, const void* src, uint64_t bytes,
   import_units(st, st->seqs, h, recs, (uint64_t)(uintptr_t)src, &u);
   r = copy_units(st, u, 0, s);
   if (r != HS_OK) return r;
-  return end_call(st, s);
+  return ce.finish();
   ABI_END
 }
 
@@ -1458,6 +1481,7 @@ extern "C" hs_status hs_kv_import_many(hs_stage* st, int32_t n_blobs, const void
   hipStream_t s = pick(st, stream);
   r = begin_call(st, s);
   if (r != HS_OK) return r;
+  CallEnd ce{st, s};
   st->seqs.swap(seqs);
   st->free_blocks.swap(free_blocks);
   Units u;
@@ -1465,7 +1489,7 @@ extern "C" hs_status hs_kv_import_many(hs_stage* st, int32_t n_blobs, const void
     import_units(st, st->seqs, hs_[i], recs[i], (uint64_t)(uintptr_t)srcs[i], &u);
   r = copy_units(st, u, 0, s);
   if (r != HS_OK) return r;
-  return end_call(st, s);
+  return ce.finish();
   ABI_END
 }
 
