@@ -621,6 +621,8 @@ hs_status copy_units(hs_stage* st, const Units& u, int zero_tail, hipStream_t s,
   if (head) memcpy(h + o_head, head->data(), head->size());
   r = pull_desc(st, h, o_head, head, head_dst, s);
   if (r != HS_OK) return r;
+  st->cur_desc = true;  // the pull is queued: the call's end guards the buffer
+  st->desc_used = true;
   const uint64_t* dsrc = reinterpret_cast<const uint64_t*>(st->d_desc);
   const uint64_t* ddst = reinterpret_cast<const uint64_t*>(st->d_desc + o_dst);
   const int32_t* dval = reinterpret_cast<const int32_t*>(st->d_desc + o_val);
@@ -631,8 +633,6 @@ hs_status copy_units(hs_stage* st, const Units& u, int zero_tail, hipStream_t s,
     });
     if (r != HS_OK) return r;
   }
-  st->cur_desc = true;
-  st->desc_used = true;
   return HS_OK;
 }
 
